@@ -1,0 +1,189 @@
+"""CPU oracle for the ragged transformer encoder layer (test infrastructure only).
+
+Only the tests, ``__graft_entry__.smoke()`` and the CPU-baseline leg of
+``bench.py`` may import this package.  The product library never does: the GPU
+path shares no code with it.  The arithmetic lives in ``oracle.c`` (plain C,
+double-precision accumulation); this module only marshals numpy arrays.
+
+Every function takes and returns *storage* arrays: float32 for dtype "f32",
+uint16 bfloat16 bit patterns for dtype "bf16".
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "oracle.c")
+_LIB = os.path.join(_HERE, "liboracle.so")
+
+F32, BF16 = 0, 1
+ACT_NONE, ACT_GELU_ERF, ACT_GELU_TANH = 0, 1, 2
+_DT = {"f32": F32, "bf16": BF16, F32: F32, BF16: BF16}
+
+
+def build(force: bool = True) -> str:
+    """Compile oracle.c into liboracle.so with gcc (strict IEEE: no fast-math,
+    no FMA contraction)."""
+    if force or not os.path.exists(_LIB):
+        tmp = _LIB + ".tmp"
+        subprocess.check_call([
+            "gcc", "-O2", "-std=gnu11", "-fPIC", "-shared", "-ffp-contract=off",
+            "-fno-fast-math", "-Wall", "-o", tmp, _SRC, "-lm"])
+        os.replace(tmp, _LIB)
+    return _LIB
+
+
+_lib = None
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB):
+            build()
+        l = ctypes.CDLL(_LIB)
+        p, i32, i64, f64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_double
+        l.oracle_offsets.restype = ctypes.c_int
+        l.oracle_offsets.argtypes = [i32, p, i32, i32, i32, p, p, p, p, p, p, p, i64, p, i64, p]
+        l.oracle_qkt.argtypes = [ctypes.c_int, i32, p, i32, i32, p, i64, p, i64, f64, p]
+        l.oracle_softmax.argtypes = [ctypes.c_int, i32, p, i32, p, p]
+        l.oracle_attn_v.argtypes = [ctypes.c_int, i32, p, i32, i32, p, p, i64, p, i64]
+        l.oracle_linear.argtypes = [ctypes.c_int, i64, i32, i32, p, i64, p, p, p, i64, ctypes.c_int, p, i64]
+        l.oracle_layernorm.argtypes = [ctypes.c_int, i64, i32, p, i64, p, p, f64, p, i64]
+        l.oracle_encoder_layer.restype = ctypes.c_int
+        l.oracle_encoder_layer.argtypes = [ctypes.c_int, i32, p, i32, i32, i32, f64, ctypes.c_int, p, p, p]
+        l.oracle_round_bf16.argtypes = [i64, p, p]
+        _lib = l
+    return _lib
+
+
+def _ptr(a):
+    return None if a is None else a.ctypes.data_as(ctypes.c_void_p)
+
+
+def _storage_dtype(dtype):
+    return np.float32 if _DT[dtype] == F32 else np.uint16
+
+
+def _lens(lengths):
+    return np.ascontiguousarray(lengths, dtype=np.int32)
+
+
+def round_bf16(x: np.ndarray) -> np.ndarray:
+    """Round float64 values to bfloat16 bits (round to nearest, ties to even)."""
+    x = np.ascontiguousarray(x, dtype=np.float64)
+    out = np.empty(x.shape, dtype=np.uint16)
+    lib().oracle_round_bf16(x.size, _ptr(x), _ptr(out))
+    return out
+
+
+class Plan:
+    """The prelude's arrays, as computed by the oracle."""
+
+    def __init__(self, tok_off, att_off, order, tok_seq, qkt_item_off, av_item_off,
+                 qkt_items, av_items, rc):
+        self.tok_off, self.att_off, self.order, self.tok_seq = tok_off, att_off, order, tok_seq
+        self.qkt_item_off, self.av_item_off = qkt_item_off, av_item_off
+        self.qkt_items, self.av_items, self.rc = qkt_items, av_items, rc
+
+
+def offsets(lengths, heads: int, tile_m: int = 64, tile_n: int = 64,
+            qkt_cap: int | None = None, av_cap: int | None = None) -> Plan:
+    L = _lens(lengths)
+    B = L.size
+    T = int(max(L.sum(), 0))
+    if qkt_cap is None:
+        qkt_cap = int(sum(heads * (-(-max(int(v), 0) // tile_m)) * (-(-max(int(v), 0) // tile_n)) for v in L))
+    if av_cap is None:
+        av_cap = int(sum(heads * (-(-max(int(v), 0) // tile_m)) for v in L))
+    tok_off = np.zeros(B + 1, np.int64)
+    att_off = np.zeros(B + 1, np.int64)
+    order = np.zeros(B, np.int32)
+    tok_seq = np.zeros(max(T, 1), np.int32)
+    qoff = np.zeros(B + 1, np.int64)
+    aoff = np.zeros(B + 1, np.int64)
+    qitems = np.zeros(max(4 * qkt_cap, 4), np.int32)
+    aitems = np.zeros(max(3 * av_cap, 3), np.int32)
+    counts = np.zeros(2, np.int64)
+    rc = lib().oracle_offsets(B, _ptr(L), heads, tile_m, tile_n, _ptr(tok_off), _ptr(att_off),
+                              _ptr(order), _ptr(tok_seq), _ptr(qoff), _ptr(aoff),
+                              _ptr(qitems), qkt_cap, _ptr(aitems), av_cap, _ptr(counts))
+    nq, na = int(counts[0]), int(counts[1])
+    return Plan(tok_off, att_off, order, tok_seq[:T], qoff, aoff,
+                qitems[:4 * min(nq, qkt_cap)].reshape(-1, 4), aitems[:3 * min(na, av_cap)].reshape(-1, 3), rc)
+
+
+def score_elems(lengths, heads: int) -> int:
+    L = _lens(lengths).astype(np.int64)
+    return int(heads * (L * L).sum())
+
+
+def qkt(dtype, lengths, heads, head_dim, q, ldq, k, ldk, scale):
+    L = _lens(lengths)
+    S = np.zeros(max(score_elems(L, heads), 1), _storage_dtype(dtype))
+    lib().oracle_qkt(_DT[dtype], L.size, _ptr(L), heads, head_dim, _ptr(np.ascontiguousarray(q)), ldq,
+                     _ptr(np.ascontiguousarray(k)), ldk, float(scale), _ptr(S))
+    return S[:score_elems(L, heads)]
+
+
+def softmax(dtype, lengths, heads, S):
+    L = _lens(lengths)
+    S = np.ascontiguousarray(S)
+    P = np.zeros(max(S.size, 1), _storage_dtype(dtype))
+    lib().oracle_softmax(_DT[dtype], L.size, _ptr(L), heads, _ptr(S), _ptr(P))
+    return P[:S.size]
+
+
+def attn_v(dtype, lengths, heads, head_dim, P, v, ldv, ldo=None):
+    L = _lens(lengths)
+    T = int(L.sum())
+    ldo = heads * head_dim if ldo is None else ldo
+    O = np.zeros(max(T * ldo, 1), _storage_dtype(dtype))
+    lib().oracle_attn_v(_DT[dtype], L.size, _ptr(L), heads, head_dim, _ptr(np.ascontiguousarray(P)),
+                        _ptr(np.ascontiguousarray(v)), ldv, _ptr(O), ldo)
+    return O[:T * ldo].reshape(T, ldo)
+
+
+def linear(dtype, x, w, bias=None, residual=None, act=ACT_NONE):
+    """y = act(x w^T + bias) + residual over the rows of x (all arrays in storage form)."""
+    x = np.ascontiguousarray(x)
+    w = np.ascontiguousarray(w)
+    T, K = x.shape
+    N = w.shape[0]
+    assert w.shape[1] == K
+    y = np.zeros((T, N), _storage_dtype(dtype))
+    r = None if residual is None else np.ascontiguousarray(residual)
+    b = None if bias is None else np.ascontiguousarray(bias)
+    lib().oracle_linear(_DT[dtype], T, K, N, _ptr(x), K, _ptr(w), _ptr(b), _ptr(r), N, act, _ptr(y), N)
+    return y
+
+
+def layernorm(dtype, x, gamma, beta, eps=1e-5):
+    x = np.ascontiguousarray(x)
+    T, d = x.shape
+    y = np.zeros((T, d), _storage_dtype(dtype))
+    lib().oracle_layernorm(_DT[dtype], T, d, _ptr(x), d, _ptr(np.ascontiguousarray(gamma)),
+                           _ptr(np.ascontiguousarray(beta)), float(eps), _ptr(y), d)
+    return y
+
+
+_WNAMES = ("w_qkv", "b_qkv", "w_o", "b_o", "ln1_g", "ln1_b", "w_ff1", "b_ff1", "w_ff2", "b_ff2", "ln2_g", "ln2_b")
+
+
+def encoder_layer(dtype, lengths, x, weights: dict, d_model, heads, d_ff, eps=1e-5, act=ACT_GELU_ERF):
+    """One post-LN encoder layer over packed tokens x [T, d_model]."""
+    L = _lens(lengths)
+    T = int(L.sum())
+    arrs = [np.ascontiguousarray(weights[n]) for n in _WNAMES]
+    wstruct = (ctypes.c_void_p * 12)(*[a.ctypes.data for a in arrs])
+    x = np.ascontiguousarray(x)
+    out = np.zeros((max(T, 1), d_model), _storage_dtype(dtype))
+    rc = lib().oracle_encoder_layer(_DT[dtype], L.size, _ptr(L), d_model, heads, d_ff, float(eps), act,
+                                    ctypes.cast(wstruct, ctypes.c_void_p), _ptr(x), _ptr(out))
+    if rc != 0:
+        raise MemoryError("oracle_encoder_layer: allocation failed")
+    return out[:T]
