@@ -1,0 +1,293 @@
+"""Benchmark of the ragged encoder layer on one MI355X.
+
+One step = one pass of the whole hot path over one synthetic batch: the
+prelude (ragged_offsets) followed by one encoder layer (QKV projection, fused
+ragged attention, output projection + residual, LayerNorm, FF1 + GELU,
+FF2 + residual, LayerNorm).  The workload is the batch-128 layer: lengths
+uniform in [32, 512], d_model 1024, 16 heads of 64, FFN 4096, bf16, seeded
+synthetic data and random-initialised weights (std 0.02).
+
+Prints ONE JSON line (rank 0, N = 1).  Per-kernel times come from HIP events
+recorded by the library on the stream the kernels run on; the CPU baseline
+times the oracle on a bounded sample of the same batch.
+"""
+from __future__ import annotations
+
+import argparse
+import ctypes
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
+METRIC = "ms/encoder layer + useful (unpadded) TFLOP/s, fraction of bf16 MFMA peak"
+
+# stage index (events[k] .. events[k+1]) -> kernel symbol
+STAGES = ["qkv_proj", "qkt", "softmax", "attention", "out_proj", "layernorm1", "ff1", "ff2", "layernorm2"]
+STAGE_KERNEL = {
+    "qkv_proj": "k_gemm_bf16<0, true, false>",
+    "attention": "k_attention_bf16",
+    "out_proj": "k_gemm_bf16<0, true, true>",
+    "ff2": "k_gemm_bf16<0, true, true>",
+    "ff1": "k_gemm_bf16<1, true, false>",
+    "layernorm1": "k_layernorm<true, 2>",
+    "layernorm2": "k_layernorm<true, 2>",
+}
+KERNEL_SOURCES = {
+    "k_gemm_bf16": "paper_2110_10221_amd/csrc/gemm.hip",
+    "k_attention_bf16": "paper_2110_10221_amd/csrc/attention.hip",
+    "k_layernorm": "paper_2110_10221_amd/csrc/layernorm.hip",
+}
+
+
+def stage_work(T, d, H, dff, s2):
+    """Algorithmic FLOPs and HBM bytes (bf16) of each stage: every operand read
+    once, every result written once."""
+    e = 2
+    return {
+        "qkv_proj": (2.0 * T * d * 3 * d, e * (T * d + 3 * d * d + 3 * d + T * 3 * d)),
+        "attention": (4.0 * d * s2, e * (3 * T * d + T * d)),
+        "out_proj": (2.0 * T * d * d, e * (T * d + d * d + d + 2 * T * d)),
+        "layernorm1": (8.0 * T * d, e * (2 * T * d + 2 * d)),
+        "ff1": (2.0 * T * d * dff, e * (T * d + dff * d + dff + T * dff)),
+        "ff2": (2.0 * T * dff * d, e * (T * dff + d * dff + d + 2 * T * d)),
+        "layernorm2": (8.0 * T * d, e * (2 * T * d + 2 * d)),
+    }
+
+
+def useful_flops(L, d, dff):
+    L = np.asarray(L, np.float64)
+    T, s2 = L.sum(), (L * L).sum()
+    return 2 * T * d * (3 * d + d + 2 * dff) + 4 * d * s2
+
+
+def padded_fraction(L, d, dff):
+    Lp = np.full(len(L), float(np.max(L)))
+    return 1.0 - useful_flops(L, d, dff) / useful_flops(Lp, d, dff)
+
+
+def source_hash(path):
+    return hashlib.sha256(open(os.path.join(ROOT, path), "rb").read()).hexdigest()[:16]
+
+
+def load_traffic(kernel):
+    """HBM bytes per launch measured with rocprofv3 counters (profiles/traffic.json),
+    only while the kernel's source is unchanged since the measurement."""
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    if not os.path.exists(path):
+        return None
+    try:
+        rec = json.load(open(path)).get(kernel)
+    except (OSError, ValueError):
+        return None
+    if not rec:
+        return None
+    src = KERNEL_SOURCES.get(kernel.split("<")[0])
+    if src is None or rec.get("source_sha") != source_hash(src):
+        return None
+    return rec.get("bytes_per_launch")
+
+
+class HipEvents:
+    """hipEvent_t handles from the HIP runtime torch already loaded."""
+
+    def __init__(self):
+        self.hip = ctypes.CDLL("libamdhip64.so.7")
+        self.hip.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p, ctypes.c_void_p]
+
+    def create(self, n):
+        arr = (ctypes.c_void_p * n)()
+        for i in range(n):
+            ev = ctypes.c_void_p()
+            assert self.hip.hipEventCreate(ctypes.byref(ev)) == 0
+            arr[i] = ev.value
+        return arr
+
+    def record(self, ev, stream):
+        assert self.hip.hipEventRecord(ctypes.c_void_p(ev), ctypes.c_void_p(stream)) == 0
+
+    def elapsed(self, a, b):
+        ms = ctypes.c_float()
+        assert self.hip.hipEventElapsedTime(ctypes.byref(ms), ctypes.c_void_p(a), ctypes.c_void_p(b)) == 0
+        return ms.value
+
+    def destroy(self, arr):
+        for ev in arr:
+            self.hip.hipEventDestroy(ctypes.c_void_p(ev))
+
+
+def cpu_baseline(wl, target_flops):
+    """Time the oracle's encoder layer on the first sequences of the batch whose
+    useful FLOPs reach `target_flops` (single thread)."""
+    import oracle
+    from workloads import BIAS_NAMES, LN_NAMES, WEIGHT_NAMES
+
+    cfg = wl.cfg
+    L = wl.lengths
+    n, acc = 0, 0.0
+    while n < len(L) and acc < target_flops:
+        acc += useful_flops(L[n:n + 1], cfg.d_model, cfg.d_ff)
+        n += 1
+    Ls = L[:n]
+    x = wl.tensors["x"][:int(Ls.sum())]
+    w = {k: wl.tensors[k] for k in WEIGHT_NAMES + BIAS_NAMES + LN_NAMES}
+    t0 = time.perf_counter()
+    oracle.encoder_layer("bf16", Ls, x, w, cfg.d_model, cfg.heads, cfg.d_ff)
+    dt = time.perf_counter() - t0
+    fl = useful_flops(Ls, cfg.d_model, cfg.d_ff)
+    return {"value": round(fl / dt / 1e12, 6), "unit": "TFLOP/s", "cores": 1, "kind": "oracle",
+            "sample": f"first {n} of {len(L)} sequences ({int(Ls.sum())} tokens), full layer, same weights; "
+                      f"{dt:.1f} s for {fl:.3g} useful FLOP; host has {os.cpu_count()} logical CPUs, oracle is single-threaded",
+            "ms_per_layer_extrapolated": round(useful_flops(L, cfg.d_model, cfg.d_ff) / (fl / dt) * 1e3, 1)}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--config", type=int, default=4)
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--flags", type=int, default=0, help="encoder_layer flags (1 = unfused attention)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-target-flops", type=float, default=2.0e10)
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on exactly one GPU; --gpus {args.gpus} is not supported "
+              "(the build targets a single MI355X; sharding is a design note only)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    import paper_2110_10221_amd as rag
+    from tests.helpers import dev
+    from workloads import BIAS_NAMES, LN_NAMES, WEIGHT_NAMES, make_workload
+
+    torch.cuda.set_device(0)
+    wl = make_workload(args.config, seed=args.seed)
+    cfg = wl.cfg
+    L = wl.lengths
+    T, d, H, dff = wl.total_tokens, cfg.d_model, cfg.heads, cfg.d_ff
+    s2 = float((L.astype(np.float64) ** 2).sum())
+    max_len = cfg.max_len
+    lens = torch.from_numpy(L).cuda()
+    plan = rag.Plan(lens, T, max_len, H)
+    x = dev(wl.tensors["x"], "bf16")
+    wd = {n: dev(wl.tensors[n], "bf16") for n in WEIGHT_NAMES + BIAS_NAMES + LN_NAMES}
+    wstruct = rag.layer_weights(wd)
+    ws = torch.empty(rag.encoder_layer_workspace(T, max_len, d, H, dff, rag.RAG_BF16, args.flags),
+                     dtype=torch.uint8, device="cuda")
+    y = torch.empty(T, d, dtype=torch.bfloat16, device="cuda")
+    stream = torch.cuda.current_stream()
+    sh = stream.cuda_stream
+    hip = HipEvents()
+    n_ev = rag.RAG_LAYER_EVENTS
+
+    def step(ev=None, pre=None):
+        if pre is not None:
+            hip.record(pre, sh)
+        rag.ragged_offsets(plan)
+        rag.encoder_layer(plan, x, y, wstruct, dff, ws, flags=args.flags, events=ev)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    assert not plan.data_errors(), plan.data_errors()
+
+    events = [hip.create(n_ev) for _ in range(args.steps)]
+    pre = hip.create(args.steps)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for k in range(args.steps):
+        step(events[k], pre[k])
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    ms_step = elapsed * 1e3 / args.steps
+
+    stage_ms = {s: 0.0 for s in STAGES}
+    prelude_ms = 0.0
+    for k in range(args.steps):
+        prelude_ms += hip.elapsed(pre[k], events[k][0])
+        for i, s in enumerate(STAGES):
+            stage_ms[s] += hip.elapsed(events[k][i], events[k][i + 1])
+    stage_ms = {s: v / args.steps for s, v in stage_ms.items()}
+    prelude_ms /= args.steps
+    for arr in events:
+        hip.destroy(arr)
+    hip.destroy(pre)
+
+    uf = useful_flops(L, d, dff)
+    work = stage_work(T, d, H, dff, s2)
+    # group stages by kernel symbol; the dominant kernel has the largest total time
+    per_kernel = {}
+    for s, kname in STAGE_KERNEL.items():
+        fl, by = work[s]
+        pk = per_kernel.setdefault(kname, {"ms": 0.0, "flops": 0.0, "bytes": 0.0, "launches": 0})
+        pk["ms"] += stage_ms[s]
+        pk["flops"] += fl
+        pk["bytes"] += by
+        pk["launches"] += 1
+    dom = max(per_kernel, key=lambda k: per_kernel[k]["ms"])
+    pk = per_kernel[dom]
+    avg_ms = pk["ms"] / pk["launches"]
+    if dom.startswith("k_gemm") or dom.startswith("k_attention"):
+        achieved = pk["flops"] / pk["launches"] / (avg_ms * 1e-3) / 1e12
+        roof = {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                "frac": round(achieved / PEAK_BF16_TFLOPS, 4)}
+    else:
+        achieved = pk["bytes"] / pk["launches"] / (avg_ms * 1e-3) / 1e9
+        roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                "frac": round(achieved / PEAK_HBM_GBS, 4)}
+    roof["traffic"] = load_traffic(dom)
+    roof["kernel"] = dom
+    roof["avg_launch_ms"] = round(avg_ms, 5)
+    roof["launches_per_step"] = pk["launches"]
+
+    gemm_ms = sum(stage_ms[s] for s in ("qkv_proj", "out_proj", "ff1", "ff2"))
+    gemm_fl = sum(work[s][0] for s in ("qkv_proj", "out_proj", "ff1", "ff2"))
+    attn_ms = sum(stage_ms[s] for s in ("qkt", "softmax", "attention"))
+    out = {
+        "metric": METRIC,
+        "value": round(uf / (ms_step * 1e-3) / 1e12, 2),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": f"ragged encoder layer, batch {cfg.batch}, lengths uniform [32, 512] (seed {args.seed}), "
+                               f"d_model {d}, {H} heads x 64, FFN {dff}, GELU, post-LN",
+                   "global_batch": cfg.batch, "total_tokens": T, "max_len": int(L.max()),
+                   "parallelism": "single GPU", "attention": "unfused" if args.flags & 1 else "fused"},
+        "ms_per_layer": round(ms_step, 4),
+        "ms_per_layer_prelude_amortised_6_layers": round(ms_step - prelude_ms * 5 / 6, 4),
+        "useful_tflop_per_layer": round(uf / 1e12, 4),
+        "frac_of_bf16_peak": round(uf / (ms_step * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
+        "padded_fraction": round(padded_fraction(L, d, dff), 4),
+        "gemm_tflops": round(gemm_fl / (gemm_ms * 1e-3) / 1e12, 1),
+        "gemm_frac_of_peak": round(gemm_fl / (gemm_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
+        "attention_tflops": round(work["attention"][0] / (attn_ms * 1e-3) / 1e12, 1) if attn_ms > 0 else None,
+        "stage_ms": {**{"prelude": round(prelude_ms, 4)}, **{s: round(v, 4) for s, v in stage_ms.items()}},
+        "roofline": roof,
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(wl, args.cpu_target_flops)
+    else:
+        out["cpu_baseline"] = None
+    print(json.dumps(out))
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,586 @@
+// Ragged scaled dot-product attention as three operators over the plan's work
+// lists (the paper's QK^T, Softmax and AttnV operators):
+//   ragged QK^T     one workgroup item = one 64x64 score tile of one sequence and
+//                   head; the tile never crosses a sequence boundary, so no
+//                   padded work is done beyond the predicated edge tile
+//   ragged softmax  one wave per token: the token's H rows (each L_b scores)
+//                   are contiguous in the X[b][i][h][j] layout
+//   ragged Attn.V   one workgroup item = 64 query rows of one sequence and head,
+//                   reducing over that sequence's L_b keys
+// Persistent grids walk the lists in order: sequences longest first.
+//
+// bf16 kernels use v_mfma_f32_16x16x32_bf16.  In a 16x16x32 MFMA lane l supplies
+// row (l % 16) of A and column (l % 16) of B, each with the 8 consecutive k values
+// 8*(l/16) .. 8*(l/16)+7, and receives C rows 4*(l/16) .. 4*(l/16)+3 of column l % 16.
+#include <cfloat>
+
+#include "device_common.h"
+#include "launch.h"
+
+namespace rag {
+namespace {
+
+struct PlanArgs {
+    const int32_t* lengths;
+    const int32_t* tok_off;
+    const int64_t* att_off;
+    const int32_t* tok_seq;
+    const int32_t* qkt_items;
+    const int32_t* av_items;
+    int32_t* status;
+    int batch, heads;
+};
+
+PlanArgs plan_args(const PlanView& p) {
+    return PlanArgs{p.lengths, p.tok_off, p.att_off, p.tok_seq, p.qkt_items, p.av_items, p.status,
+                    p.batch, p.heads};
+}
+
+// True if the plan is valid and the score buffer large enough; otherwise one
+// thread records the overflow and every workgroup returns.
+__device__ __forceinline__ bool plan_ok(const PlanArgs& pa, int64_t score_cap) {
+    if (pa.status[0] != 0) return false;
+    if (pa.att_off[pa.batch] > score_cap) {
+        if (blockIdx.x == 0 && threadIdx.x == 0) atomicOr(pa.status, kDataScoreCap);
+        return false;
+    }
+    return true;
+}
+
+__device__ __forceinline__ u32x4 ld16(const uint16_t* p) { return *reinterpret_cast<const u32x4*>(p); }
+
+// ---------------------------------------------------------------------------
+// QK^T
+// ---------------------------------------------------------------------------
+
+constexpr int kStage = kTile + 8;  // padded LDS row (elements)
+
+__global__ __launch_bounds__(256) void k_qkt_bf16(PlanArgs pa, const uint16_t* __restrict__ q, int ldq,
+                                                   const uint16_t* __restrict__ k, int ldk, float scale,
+                                                   uint16_t* __restrict__ S, int64_t score_cap) {
+    if (!plan_ok(pa, score_cap)) return;
+    __shared__ uint16_t tile[kTile][kStage];
+    const int n_items = pa.status[1];
+    const int H = pa.heads;
+    const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
+    const int l16 = lane % 16, q4 = lane / 16;
+    for (int it = blockIdx.x; it < n_items; it += gridDim.x) {
+        const int4 item = reinterpret_cast<const int4*>(pa.qkt_items)[it];
+        const int b = item.x, h = item.y, ti = item.z, tj = item.w;
+        const int L = pa.lengths[b];
+        const int t0 = pa.tok_off[b];
+        const int64_t base = pa.att_off[b];
+        // this wave: query rows ti*64 + wave*16 .. +15, all 64 key columns of the tile
+        const int qi = min(ti * kTile + wave * 16 + l16, L - 1);
+        const uint16_t* qrow = q + (int64_t)(t0 + qi) * ldq + h * kHeadDim + 8 * q4;
+        const bf16x8 qa0 = as_bf16x8(ld16(qrow)), qa1 = as_bf16x8(ld16(qrow + 32));
+        floatx4 acc[4];
+#pragma unroll
+        for (int jb = 0; jb < 4; ++jb) {
+            const int kj = min(tj * kTile + jb * 16 + l16, L - 1);
+            const uint16_t* krow = k + (int64_t)(t0 + kj) * ldk + h * kHeadDim + 8 * q4;
+            const bf16x8 kb0 = as_bf16x8(ld16(krow)), kb1 = as_bf16x8(ld16(krow + 32));
+            acc[jb] = floatx4{0.f, 0.f, 0.f, 0.f};
+            acc[jb] = mfma16x16x32(kb0, qa0, acc[jb]);  // C[j][i] = sum_c K[j][c] Q[i][c]
+            acc[jb] = mfma16x16x32(kb1, qa1, acc[jb]);
+        }
+        __syncthreads();  // the previous item's stores have read the staging tile
+#pragma unroll
+        for (int jb = 0; jb < 4; ++jb)
+#pragma unroll
+            for (int r = 0; r < 4; ++r)
+                tile[wave * 16 + l16][jb * 16 + 4 * q4 + r] = f32_to_bf16(acc[jb][r] * scale);
+        __syncthreads();
+        const int rows = min(kTile, L - ti * kTile), cols = min(kTile, L - tj * kTile);
+        for (int rr = wave; rr < rows; rr += 4)
+            if (lane < cols)
+                S[base + ((int64_t)(ti * kTile + rr) * H + h) * L + tj * kTile + lane] = tile[rr][lane];
+    }
+}
+
+__global__ __launch_bounds__(256) void k_qkt_f32(PlanArgs pa, const float* __restrict__ q, int ldq,
+                                                  const float* __restrict__ k, int ldk, float scale,
+                                                  float* __restrict__ S, int64_t score_cap) {
+    if (!plan_ok(pa, score_cap)) return;
+    __shared__ float Qs[kTile][kHeadDim + 1], Ks[kTile][kHeadDim + 1];
+    const int n_items = pa.status[1];
+    const int H = pa.heads;
+    const int tx = threadIdx.x % 16, ty = threadIdx.x / 16;
+    for (int it = blockIdx.x; it < n_items; it += gridDim.x) {
+        const int4 item = reinterpret_cast<const int4*>(pa.qkt_items)[it];
+        const int b = item.x, h = item.y, ti = item.z, tj = item.w;
+        const int L = pa.lengths[b];
+        const int t0 = pa.tok_off[b];
+        const int64_t base = pa.att_off[b];
+        __syncthreads();
+        for (int e = threadIdx.x; e < kTile * kHeadDim; e += 256) {
+            const int r = e / kHeadDim, c = e % kHeadDim;
+            const int qi = min(ti * kTile + r, L - 1), kj = min(tj * kTile + r, L - 1);
+            Qs[r][c] = q[(int64_t)(t0 + qi) * ldq + h * kHeadDim + c];
+            Ks[r][c] = k[(int64_t)(t0 + kj) * ldk + h * kHeadDim + c];
+        }
+        __syncthreads();
+        float acc[4][4] = {};
+        for (int c = 0; c < kHeadDim; ++c) {
+            float a[4], bb[4];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                a[u] = Qs[ty * 4 + u][c];
+                bb[u] = Ks[tx + 16 * u][c];
+            }
+#pragma unroll
+            for (int u = 0; u < 4; ++u)
+#pragma unroll
+                for (int v = 0; v < 4; ++v) acc[u][v] = fmaf(a[u], bb[v], acc[u][v]);
+        }
+        const int rows = min(kTile, L - ti * kTile), cols = min(kTile, L - tj * kTile);
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const int i = ty * 4 + u;
+            if (i >= rows) continue;
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+                const int j = tx + 16 * v;
+                if (j < cols) S[base + ((int64_t)(ti * kTile + i) * H + h) * L + tj * kTile + j] = acc[u][v] * scale;
+            }
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Softmax
+// ---------------------------------------------------------------------------
+
+template <bool BF16>
+struct Elem;
+template <>
+struct Elem<true> {
+    using T = uint16_t;
+    static __device__ __forceinline__ float load(const T* p) { return bf16_to_f32(*p); }
+    static __device__ __forceinline__ void store(T* p, float v) { *p = f32_to_bf16(v); }
+    static __device__ __forceinline__ float exp(float x) { return __expf(x); }
+};
+template <>
+struct Elem<false> {
+    using T = float;
+    static __device__ __forceinline__ float load(const T* p) { return *p; }
+    static __device__ __forceinline__ void store(T* p, float v) { *p = v; }
+    static __device__ __forceinline__ float exp(float x) { return expf(x); }
+};
+
+constexpr int kSoftmaxRegs = 8;  // rows up to 64 * 8 = 512 scores stay in registers
+
+template <bool BF16>
+__global__ __launch_bounds__(256) void k_softmax(PlanArgs pa, const typename Elem<BF16>::T* S,
+                                                  typename Elem<BF16>::T* P, int64_t score_cap, int T) {
+    using E = Elem<BF16>;
+    if (!plan_ok(pa, score_cap)) return;
+    const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
+    const int t = blockIdx.x * 4 + wave;
+    if (t >= T) return;
+    const int b = pa.tok_seq[t];
+    const int L = pa.lengths[b];
+    const int H = pa.heads;
+    const int64_t row0 = pa.att_off[b] + (int64_t)(t - pa.tok_off[b]) * H * L;
+    if (L <= kWave) {
+        // 64/G rows per pass, G = next power of two >= L lanes per row
+        int G = 1;
+        while (G < L) G <<= 1;
+        const int R = kWave / G, r = lane / G, e = lane % G;
+        for (int h0 = 0; h0 < H; h0 += R) {
+            const int h = h0 + r;
+            const bool valid = (h < H) && (e < L);
+            const int64_t off = row0 + (int64_t)h * L + e;
+            const float x = valid ? E::load(S + off) : -FLT_MAX;
+            const float m = group_max(x, G);
+            const float ex = valid ? E::exp(x - m) : 0.f;
+            const float s = group_sum(ex, G);
+            if (valid) E::store(P + off, ex * (1.0f / s));
+        }
+    } else if (L <= kWave * kSoftmaxRegs) {
+        for (int h = 0; h < H; ++h) {
+            const int64_t rp = row0 + (int64_t)h * L;
+            float x[kSoftmaxRegs];
+            float m = -FLT_MAX;
+#pragma unroll
+            for (int u = 0; u < kSoftmaxRegs; ++u) {
+                const int j = lane + kWave * u;
+                x[u] = j < L ? E::load(S + rp + j) : -FLT_MAX;
+                m = fmaxf(m, x[u]);
+            }
+            m = wave_max(m);
+            float s = 0.f;
+#pragma unroll
+            for (int u = 0; u < kSoftmaxRegs; ++u) {
+                const int j = lane + kWave * u;
+                x[u] = j < L ? E::exp(x[u] - m) : 0.f;
+                s += x[u];
+            }
+            const float inv = 1.0f / wave_sum(s);
+#pragma unroll
+            for (int u = 0; u < kSoftmaxRegs; ++u) {
+                const int j = lane + kWave * u;
+                if (j < L) E::store(P + rp + j, x[u] * inv);
+            }
+        }
+    } else {
+        // long rows: max pass, sum pass, write pass (each element is read before
+        // the same lane overwrites it, so in-place use is safe)
+        for (int h = 0; h < H; ++h) {
+            const int64_t rp = row0 + (int64_t)h * L;
+            float m = -FLT_MAX;
+            for (int j = lane; j < L; j += kWave) m = fmaxf(m, E::load(S + rp + j));
+            m = wave_max(m);
+            float s = 0.f;
+            for (int j = lane; j < L; j += kWave) s += E::exp(E::load(S + rp + j) - m);
+            const float inv = 1.0f / wave_sum(s);
+            for (int j = lane; j < L; j += kWave) E::store(P + rp + j, E::exp(E::load(S + rp + j) - m) * inv);
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Attn.V
+// ---------------------------------------------------------------------------
+
+__global__ __launch_bounds__(256) void k_attn_v_bf16(PlanArgs pa, const uint16_t* __restrict__ P,
+                                                      int64_t score_cap, const uint16_t* __restrict__ v,
+                                                      int ldv, uint16_t* __restrict__ O, int ldo) {
+    if (!plan_ok(pa, score_cap)) return;
+    __shared__ __attribute__((aligned(16))) uint16_t Ps[kTile][kStage];  // [i][j]
+    __shared__ __attribute__((aligned(16))) uint16_t Vt[kTile][kStage];  // [c][j]
+    const int n_items = pa.status[2];
+    const int H = pa.heads;
+    const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
+    const int l16 = lane % 16, q4 = lane / 16;
+    for (int it = blockIdx.x; it < n_items; it += gridDim.x) {
+        const int b = pa.av_items[3 * it], h = pa.av_items[3 * it + 1], ti = pa.av_items[3 * it + 2];
+        const int L = pa.lengths[b];
+        const int t0 = pa.tok_off[b];
+        const int64_t base = pa.att_off[b];
+        const int rows = min(kTile, L - ti * kTile);
+        floatx4 acc[4];
+#pragma unroll
+        for (int cb = 0; cb < 4; ++cb) acc[cb] = floatx4{0.f, 0.f, 0.f, 0.f};
+        for (int j0 = 0; j0 < L; j0 += kTile) {
+            const int cols = min(kTile, L - j0);
+            __syncthreads();
+            // probabilities: rows i of the tile, keys j0..j0+63 (zero outside)
+#pragma unroll 4
+            for (int r = 0; r < 16; ++r) {
+                const int i = threadIdx.x / kWave + 4 * r, j = lane;
+                uint16_t val = 0;
+                if (i < rows && j < cols) val = P[base + ((int64_t)(ti * kTile + i) * H + h) * L + j0 + j];
+                Ps[i][j] = val;
+            }
+            // values: 64 keys x 64 channels, stored transposed [c][j]
+#pragma unroll
+            for (int r = 0; r < 2; ++r) {
+                const int id = threadIdx.x + 256 * r;
+                const int jj = id >> 3, cc = (id & 7) * 8;
+                u32x4 vv = {0u, 0u, 0u, 0u};
+                if (jj < cols) vv = ld16(v + (int64_t)(t0 + j0 + jj) * ldv + h * kHeadDim + cc);
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    Vt[cc + 2 * e][jj] = static_cast<uint16_t>(vv[e] & 0xffffu);
+                    Vt[cc + 2 * e + 1][jj] = static_cast<uint16_t>(vv[e] >> 16);
+                }
+            }
+            __syncthreads();
+#pragma unroll
+            for (int ks = 0; ks < 2; ++ks) {
+                const bf16x8 pb = as_bf16x8(*reinterpret_cast<const u32x4*>(&Ps[wave * 16 + l16][32 * ks + 8 * q4]));
+#pragma unroll
+                for (int cb = 0; cb < 4; ++cb) {
+                    const bf16x8 va = as_bf16x8(*reinterpret_cast<const u32x4*>(&Vt[cb * 16 + l16][32 * ks + 8 * q4]));
+                    acc[cb] = mfma16x16x32(va, pb, acc[cb]);  // C[c][i] = sum_j V[j][c] P[i][j]
+                }
+            }
+        }
+        const int i = wave * 16 + l16;
+        if (i < rows) {
+            uint16_t* orow = O + (int64_t)(t0 + ti * kTile + i) * ldo + h * kHeadDim;
+#pragma unroll
+            for (int cb = 0; cb < 4; ++cb) {
+                u32x2 w2 = {pack_bf16x2(acc[cb][0], acc[cb][1]), pack_bf16x2(acc[cb][2], acc[cb][3])};
+                *reinterpret_cast<u32x2*>(orow + cb * 16 + 4 * q4) = w2;
+            }
+        }
+    }
+}
+
+__global__ __launch_bounds__(256) void k_attn_v_f32(PlanArgs pa, const float* __restrict__ P, int64_t score_cap,
+                                                     const float* __restrict__ v, int ldv, float* __restrict__ O,
+                                                     int ldo) {
+    if (!plan_ok(pa, score_cap)) return;
+    __shared__ float Ps[kTile][kTile + 1], Vs[kTile][kHeadDim + 1];
+    const int n_items = pa.status[2];
+    const int H = pa.heads;
+    const int tx = threadIdx.x % 16, ty = threadIdx.x / 16;
+    for (int it = blockIdx.x; it < n_items; it += gridDim.x) {
+        const int b = pa.av_items[3 * it], h = pa.av_items[3 * it + 1], ti = pa.av_items[3 * it + 2];
+        const int L = pa.lengths[b];
+        const int t0 = pa.tok_off[b];
+        const int64_t base = pa.att_off[b];
+        const int rows = min(kTile, L - ti * kTile);
+        float acc[4][4] = {};
+        for (int j0 = 0; j0 < L; j0 += kTile) {
+            const int cols = min(kTile, L - j0);
+            __syncthreads();
+            for (int e = threadIdx.x; e < kTile * kTile; e += 256) {
+                const int r = e / kTile, c = e % kTile;
+                Ps[r][c] = (r < rows && c < cols) ? P[base + ((int64_t)(ti * kTile + r) * H + h) * L + j0 + c] : 0.f;
+                Vs[r][c] = r < cols ? v[(int64_t)(t0 + j0 + r) * ldv + h * kHeadDim + c] : 0.f;
+            }
+            __syncthreads();
+            for (int j = 0; j < kTile; ++j) {
+                float a[4], bb[4];
+#pragma unroll
+                for (int u = 0; u < 4; ++u) {
+                    a[u] = Ps[ty * 4 + u][j];
+                    bb[u] = Vs[j][tx + 16 * u];
+                }
+#pragma unroll
+                for (int u = 0; u < 4; ++u)
+#pragma unroll
+                    for (int w = 0; w < 4; ++w) acc[u][w] = fmaf(a[u], bb[w], acc[u][w]);
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const int i = ty * 4 + u;
+            if (i >= rows) continue;
+#pragma unroll
+            for (int w = 0; w < 4; ++w)
+                O[(int64_t)(t0 + ti * kTile + i) * ldo + h * kHeadDim + tx + 16 * w] = acc[u][w];
+        }
+    }
+}
+
+
+// ---------------------------------------------------------------------------
+// Fused ragged attention: QK^T, softmax and Attn.V of one item (sequence b,
+// head h, 64 query rows) in one workgroup, with the same rounding points as the
+// three separate operators: scores rounded to bf16, an exact two-pass softmax
+// (row max and row sum over all of the sequence's keys first), probabilities
+// rounded to bf16, fp32 accumulation of P.V.  Each wave owns 16 query rows and
+// keeps their bf16 scores packed in registers (up to kFusedMaxTiles key tiles,
+// i.e. rows of up to 512 keys), so the H * sum L_b^2 scores never reach memory.
+//   pass 1  stream the sequence's K tiles:   S^T tile C[j][i] = sum_c K[j][c] Q[i][c];
+//           lane holds row i = lane % 16, keys j = jb*16 + 4*(lane/16) + r
+//   pass 2  stream the V tiles:               O^T C[c][i] = sum_j V[j][c] P[i][j]
+//           with P straight from registers: the MFMA pairs the k-th element of A
+//           with the k-th element of B, so the lane's keys {4q..4q+3, 16+4q..16+4q+3}
+//           of each 32-key step serve as its 8 k values and the V operand is read
+//           for the same keys.
+// K tiles sit in LDS as [j][c] (16-byte chunks XOR-swizzled by row), V tiles
+// transposed as [c][j]; both double-buffered, the next tile's global loads in
+// flight while the current one is used.
+// ---------------------------------------------------------------------------
+
+constexpr int kFusedMaxTiles = 8;  // longest supported sequence: 8 * 64 = 512 keys
+
+__device__ __forceinline__ float bf16_round(float x) { return bf16_to_f32(f32_to_bf16(x)); }
+
+struct Row16 {
+    u32x4 a, b;
+};
+
+// 16 channels (starting at column `col`) of key row j of a sequence starting at
+// token t0; rows past the sequence read its last row and come back as zeros.
+__device__ __forceinline__ Row16 fetch_row16(const uint16_t* base, int ld, int t0, int j, int L, int col) {
+    const uint16_t* p = base + (int64_t)(t0 + min(j, L - 1)) * ld + col;
+    Row16 r{ld16(p), ld16(p + 8)};
+    if (j >= L) r.a = r.b = u32x4{0u, 0u, 0u, 0u};
+    return r;
+}
+
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k_attention_bf16(PlanArgs pa, const uint16_t* __restrict__ q, int ldq,
+                                                         const uint16_t* __restrict__ k, int ldk,
+                                                         const uint16_t* __restrict__ v, int ldv, float scale,
+                                                         uint16_t* __restrict__ O, int ldo) {
+    if (pa.status[0] != 0) return;
+    __shared__ __attribute__((aligned(16))) uint16_t Ks[2][kTile * kHeadDim];
+    __shared__ __attribute__((aligned(16))) uint16_t Vt[2][kHeadDim][kStage];
+    const int n_items = pa.status[2];
+    const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
+    const int l16 = lane % 16, q4 = lane / 16;
+    const int ld_row = threadIdx.x >> 2, ld_c = (threadIdx.x & 3) * 16;  // loader: 16 channels of one key
+    for (int it = blockIdx.x; it < n_items; it += gridDim.x) {
+        const int b = pa.av_items[3 * it], h = pa.av_items[3 * it + 1], ti = pa.av_items[3 * it + 2];
+        const int L = pa.lengths[b];
+        const int t0 = pa.tok_off[b];
+        const int nkt = (L + kTile - 1) / kTile;
+        const int qi = min(ti * kTile + wave * 16 + l16, L - 1);
+        const uint16_t* qrow = q + (int64_t)(t0 + qi) * ldq + h * kHeadDim + 8 * q4;
+        const bf16x8 qa0 = as_bf16x8(ld16(qrow)), qa1 = as_bf16x8(ld16(qrow + 32));
+
+        Row16 rw;  // one key's 16 channels in flight (K in pass 1, V in pass 2)
+        auto store_k = [&](int buf) {
+            const int c0 = ld_c / 8;
+            *reinterpret_cast<u32x4*>(&Ks[buf][ld_row * kHeadDim + ((c0 ^ (ld_row & 7)) * 8)]) = rw.a;
+            *reinterpret_cast<u32x4*>(&Ks[buf][ld_row * kHeadDim + (((c0 + 1) ^ (ld_row & 7)) * 8)]) = rw.b;
+        };
+        auto store_v = [&](int buf) {
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                Vt[buf][ld_c + 2 * e][ld_row] = static_cast<uint16_t>(rw.a[e] & 0xffffu);
+                Vt[buf][ld_c + 2 * e + 1][ld_row] = static_cast<uint16_t>(rw.a[e] >> 16);
+                Vt[buf][ld_c + 8 + 2 * e][ld_row] = static_cast<uint16_t>(rw.b[e] & 0xffffu);
+                Vt[buf][ld_c + 8 + 2 * e + 1][ld_row] = static_cast<uint16_t>(rw.b[e] >> 16);
+            }
+        };
+
+        // ---- pass 1: bf16 scores of this wave's 16 rows, packed in registers
+        uint32_t sp[kFusedMaxTiles][8];  // [tile][jb*2 + pair]: keys jb*16 + 4*q4 + {0,1} / {2,3}
+        float mrow = -INFINITY;
+        rw = fetch_row16(k, ldk, t0, ld_row, L, h * kHeadDim + ld_c);
+        __syncthreads();  // the previous item is done with the LDS buffers
+        store_k(0);
+        __syncthreads();
+#pragma unroll
+        for (int kt = 0; kt < kFusedMaxTiles; ++kt) {
+            if (kt < nkt) {
+                const int cur = kt & 1;
+                if (kt + 1 < nkt) rw = fetch_row16(k, ldk, t0, (kt + 1) * kTile + ld_row, L, h * kHeadDim + ld_c);
+#pragma unroll
+                for (int jb = 0; jb < 4; ++jb) {
+                    const int r = jb * 16 + l16;
+                    const bf16x8 k0 = as_bf16x8(*reinterpret_cast<const u32x4*>(&Ks[cur][r * kHeadDim + ((q4 ^ (r & 7)) * 8)]));
+                    const bf16x8 k1 =
+                        as_bf16x8(*reinterpret_cast<const u32x4*>(&Ks[cur][r * kHeadDim + (((4 + q4) ^ (r & 7)) * 8)]));
+                    floatx4 st = {0.f, 0.f, 0.f, 0.f};
+                    st = mfma16x16x32(k0, qa0, st);
+                    st = mfma16x16x32(k1, qa1, st);
+                    float sv[4];
+#pragma unroll
+                    for (int rr = 0; rr < 4; ++rr) {
+                        const int j = kt * kTile + jb * 16 + 4 * q4 + rr;
+                        sv[rr] = j < L ? bf16_round(st[rr] * scale) : -INFINITY;
+                        mrow = fmaxf(mrow, sv[rr]);
+                    }
+                    sp[kt][jb * 2] = pack_bf16x2(sv[0], sv[1]);
+                    sp[kt][jb * 2 + 1] = pack_bf16x2(sv[2], sv[3]);
+                }
+                if (kt + 1 < nkt) store_k(cur ^ 1);
+                __syncthreads();
+            }
+        }
+        // ---- exact softmax statistics over the whole row (4 lanes share a row)
+        mrow = fmaxf(mrow, __shfl_xor(mrow, 16, kWave));
+        mrow = fmaxf(mrow, __shfl_xor(mrow, 32, kWave));
+        float lsum = 0.f;
+#pragma unroll
+        for (int kt = 0; kt < kFusedMaxTiles; ++kt)
+            if (kt < nkt)
+#pragma unroll
+                for (int e = 0; e < 8; ++e)
+                    lsum += __expf(lo_bf16(sp[kt][e]) - mrow) + __expf(hi_bf16(sp[kt][e]) - mrow);
+        lsum += __shfl_xor(lsum, 16, kWave);
+        lsum += __shfl_xor(lsum, 32, kWave);
+        const float inv = 1.0f / lsum;
+
+        // ---- pass 2: O = P V with P = bf16(exp(S - max) / sum)
+        floatx4 acc[4];
+#pragma unroll
+        for (int cb = 0; cb < 4; ++cb) acc[cb] = floatx4{0.f, 0.f, 0.f, 0.f};
+        rw = fetch_row16(v, ldv, t0, ld_row, L, h * kHeadDim + ld_c);
+        store_v(0);
+        __syncthreads();
+#pragma unroll
+        for (int kt = 0; kt < kFusedMaxTiles; ++kt) {
+            if (kt < nkt) {
+                const int cur = kt & 1;
+                if (kt + 1 < nkt) rw = fetch_row16(v, ldv, t0, (kt + 1) * kTile + ld_row, L, h * kHeadDim + ld_c);
+#pragma unroll
+                for (int ks = 0; ks < 2; ++ks) {
+                    u32x4 pw;
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        const uint32_t sw = sp[kt][ks * 4 + e];
+                        pw[e] = pack_bf16x2(__expf(lo_bf16(sw) - mrow) * inv, __expf(hi_bf16(sw) - mrow) * inv);
+                    }
+                    const bf16x8 pb = as_bf16x8(pw);
+#pragma unroll
+                    for (int cb = 0; cb < 4; ++cb) {
+                        const uint16_t* vrow = &Vt[cur][cb * 16 + l16][32 * ks + 4 * q4];
+                        const u32x2 lo = *reinterpret_cast<const u32x2*>(vrow);
+                        const u32x2 hi = *reinterpret_cast<const u32x2*>(vrow + 16);
+                        acc[cb] = mfma16x16x32(as_bf16x8(u32x4{lo[0], lo[1], hi[0], hi[1]}), pb, acc[cb]);
+                    }
+                }
+                if (kt + 1 < nkt) store_v(cur ^ 1);
+                __syncthreads();
+            }
+        }
+        const int i = ti * kTile + wave * 16 + l16;
+        if (i < L) {
+            uint16_t* orow = O + (int64_t)(t0 + i) * ldo + h * kHeadDim;
+#pragma unroll
+            for (int cb = 0; cb < 4; ++cb) {
+                const u32x2 w2 = {pack_bf16x2(acc[cb][0], acc[cb][1]), pack_bf16x2(acc[cb][2], acc[cb][3])};
+                *reinterpret_cast<u32x2*>(orow + cb * 16 + 4 * q4) = w2;
+            }
+        }
+    }
+}
+
+int persistent_grid(int64_t cap, int per_cu) {
+    const int64_t g = (int64_t)device_cu_count() * per_cu;
+    return static_cast<int>(cap < g ? (cap > 0 ? cap : 1) : g);
+}
+
+}  // namespace
+
+hipError_t launch_qkt(const PlanView& p, int dtype, const void* q, int ldq, const void* k, int ldk, float scale,
+                      void* scores, int64_t score_cap, hipStream_t s) {
+    const PlanArgs pa = plan_args(p);
+    const int grid = persistent_grid(p.qkt_cap, 8);
+    if (dtype == 1)
+        hipLaunchKernelGGL(k_qkt_bf16, dim3(grid), dim3(256), 0, s, pa, static_cast<const uint16_t*>(q), ldq,
+                           static_cast<const uint16_t*>(k), ldk, scale, static_cast<uint16_t*>(scores), score_cap);
+    else
+        hipLaunchKernelGGL(k_qkt_f32, dim3(grid), dim3(256), 0, s, pa, static_cast<const float*>(q), ldq,
+                           static_cast<const float*>(k), ldk, scale, static_cast<float*>(scores), score_cap);
+    return hipGetLastError();
+}
+
+hipError_t launch_softmax(const PlanView& p, int dtype, const void* scores, void* probs, int64_t score_cap,
+                          hipStream_t s) {
+    if (p.total_tokens == 0) return hipSuccess;
+    const PlanArgs pa = plan_args(p);
+    const int grid = (p.total_tokens + 3) / 4;
+    if (dtype == 1)
+        hipLaunchKernelGGL(k_softmax<true>, dim3(grid), dim3(256), 0, s, pa, static_cast<const uint16_t*>(scores),
+                           static_cast<uint16_t*>(probs), score_cap, p.total_tokens);
+    else
+        hipLaunchKernelGGL(k_softmax<false>, dim3(grid), dim3(256), 0, s, pa, static_cast<const float*>(scores),
+                           static_cast<float*>(probs), score_cap, p.total_tokens);
+    return hipGetLastError();
+}
+
+hipError_t launch_attn_v(const PlanView& p, int dtype, const void* probs, int64_t score_cap, const void* v, int ldv,
+                         void* out, int ldo, hipStream_t s) {
+    const PlanArgs pa = plan_args(p);
+    const int grid = persistent_grid(p.av_cap, 8);
+    if (dtype == 1)
+        hipLaunchKernelGGL(k_attn_v_bf16, dim3(grid), dim3(256), 0, s, pa, static_cast<const uint16_t*>(probs),
+                           score_cap, static_cast<const uint16_t*>(v), ldv, static_cast<uint16_t*>(out), ldo);
+    else
+        hipLaunchKernelGGL(k_attn_v_f32, dim3(grid), dim3(256), 0, s, pa, static_cast<const float*>(probs),
+                           score_cap, static_cast<const float*>(v), ldv, static_cast<float*>(out), ldo);
+    return hipGetLastError();
+}
+
+hipError_t launch_fused_attention(const PlanView& p, int dtype, const void* q, int ldq, const void* k, int ldk,
+                                  const void* v, int ldv, float scale, void* out, int ldo, hipStream_t s) {
+    if (dtype != 1) return hipErrorInvalidValue;
+    const PlanArgs pa = plan_args(p);
+    const int grid = persistent_grid(p.av_cap, 4);
+    hipLaunchKernelGGL(k_attention_bf16, dim3(grid), dim3(256), 0, s, pa, static_cast<const uint16_t*>(q), ldq,
+                       static_cast<const uint16_t*>(k), ldk, static_cast<const uint16_t*>(v), ldv, scale,
+                       static_cast<uint16_t*>(out), ldo);
+    return hipGetLastError();
+}
+
+}  // namespace rag

@@ -1,0 +1,50 @@
+// Host-side launchers of the HIP kernels.  Each .hip file defines its kernels
+// and the launchers below; api.cpp validates arguments and calls them.  Every
+// launcher enqueues work on `stream` and returns the launch error (if any).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace rag {
+
+struct PlanView {
+    int32_t batch, total_tokens, max_len, heads;
+    int64_t qkt_cap, av_cap;
+    const int32_t* lengths;
+    int32_t* tok_off;
+    int64_t* att_off;
+    int32_t* order;
+    int32_t* tok_seq;
+    int32_t* qkt_item_off;
+    int32_t* av_item_off;
+    int32_t* qkt_items;
+    int32_t* av_items;
+    int32_t* status;
+};
+
+// Number of compute units of the current device (cached per device).
+int device_cu_count();
+
+hipError_t launch_offsets(const PlanView& p, hipStream_t s);
+
+// Attention operators; dtype 0 = fp32, 1 = bf16.  Persistent grids sized from the
+// host-side capacities; item counts are read on the device.
+hipError_t launch_qkt(const PlanView& p, int dtype, const void* q, int ldq, const void* k, int ldk,
+                      float scale, void* scores, int64_t score_cap, hipStream_t s);
+hipError_t launch_softmax(const PlanView& p, int dtype, const void* scores, void* probs,
+                          int64_t score_cap, hipStream_t s);
+hipError_t launch_attn_v(const PlanView& p, int dtype, const void* probs, int64_t score_cap,
+                         const void* v, int ldv, void* out, int ldo, hipStream_t s);
+hipError_t launch_fused_attention(const PlanView& p, int dtype, const void* q, int ldq, const void* k,
+                                  int ldk, const void* v, int ldv, float scale, void* out, int ldo,
+                                  hipStream_t s);
+
+hipError_t launch_linear(int dtype, const void* x, int ldx, const void* w, const void* bias,
+                         const void* residual, int ldr, int act, void* y, int ldy, int T, int K, int N,
+                         hipStream_t s);
+
+hipError_t launch_layernorm(int dtype, const void* x, int ldx, const void* gamma, const void* beta,
+                            float eps, void* y, int ldy, int T, int d, hipStream_t s);
+
+}  // namespace rag

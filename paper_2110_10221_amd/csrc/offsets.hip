@@ -1,0 +1,215 @@
+// The prelude on the GPU: prefix sums of the lengths, the longest-first order,
+// the token -> sequence map and the (sequence, head, tile) work lists.
+//
+// The paper builds these auxiliary arrays on the host and copies them over
+// (Section 2 pipeline; its Section 7.4 finds the copy to dominate the prelude's
+// cost).  Here the lengths already live in device memory and four small
+// kernels build everything in place, so nothing crosses PCIe:
+//   1. scan   (one workgroup): tok_off, att_off, validation, largest length
+//   2. rank   (B/256 workgroups): stable longest-first rank -> order
+//   3. items  (one workgroup): per-sequence item counts scanned in `order`
+//   4. fill   (B workgroups): work-list entries and the token map
+#include <climits>
+
+#include "device_common.h"
+#include "launch.h"
+
+namespace rag {
+namespace {
+
+constexpr int kScanThreads = 1024;
+constexpr int kScanWaves = kScanThreads / kWave;
+
+// Inclusive prefix sum across one wave (64-bit values).
+__device__ __forceinline__ int64_t wave_inclusive_scan(int64_t v, int lane) {
+#pragma unroll
+    for (int o = 1; o < kWave; o <<= 1) {
+        int64_t t = __shfl_up(v, o, kWave);
+        if (lane >= o) v += t;
+    }
+    return v;
+}
+
+// Block-wide exclusive scan of two 64-bit sequences (one value per thread);
+// returns each thread's exclusive prefixes and the block totals.  All threads
+// of the block must call it.
+__device__ __forceinline__ void block_exclusive_scan2(int64_t a, int64_t b, int64_t& ea, int64_t& eb,
+                                                      int64_t& ta, int64_t& tb, int64_t* sh_a,
+                                                      int64_t* sh_b) {
+    const int lane = threadIdx.x % kWave, wid = threadIdx.x / kWave;
+    int64_t ia = wave_inclusive_scan(a, lane);
+    int64_t ib = wave_inclusive_scan(b, lane);
+    if (lane == kWave - 1) {
+        sh_a[wid] = ia;
+        sh_b[wid] = ib;
+    }
+    __syncthreads();
+    int64_t pa = 0, pb = 0;
+    ta = 0;
+    tb = 0;
+    for (int w = 0; w < kScanWaves; ++w) {
+        if (w < wid) {
+            pa += sh_a[w];
+            pb += sh_b[w];
+        }
+        ta += sh_a[w];
+        tb += sh_b[w];
+    }
+    ea = pa + ia - a;
+    eb = pb + ib - b;
+    __syncthreads();  // the shared totals may be overwritten by the next call
+}
+
+__global__ __launch_bounds__(kScanThreads) void k_plan_scan(const int32_t* __restrict__ lengths, int B,
+                                                             int T_expected, int max_len, int H,
+                                                             int32_t* __restrict__ tok_off,
+                                                             int64_t* __restrict__ att_off,
+                                                             int32_t* __restrict__ status) {
+    __shared__ int64_t sh_a[kScanWaves], sh_b[kScanWaves];
+    __shared__ int sh_flags, sh_max;
+    if (threadIdx.x == 0) {
+        sh_flags = 0;
+        sh_max = 0;
+    }
+    __syncthreads();
+    int flags = 0, mx = 0;
+    int64_t carry_tok = 0, carry_att = 0;
+    for (int base = 0; base < B; base += kScanThreads) {
+        const int b = base + threadIdx.x;
+        int L = b < B ? lengths[b] : 0;
+        if (b < B) {
+            if (L < 0) flags |= kDataNegLength;
+            if (L > max_len) flags |= kDataLongLength;
+            mx = max(mx, L);
+        }
+        const int64_t Lc = L > 0 ? L : 0;  // negative lengths are flagged, counted as 0
+        int64_t et, ea, tt, ta;
+        block_exclusive_scan2(Lc, (int64_t)H * Lc * Lc, et, ea, tt, ta, sh_a, sh_b);
+        if (b < B) {
+            tok_off[b] = static_cast<int32_t>(carry_tok + et);
+            att_off[b] = carry_att + ea;
+        }
+        carry_tok += tt;
+        carry_att += ta;
+    }
+    if (flags) atomicOr(&sh_flags, flags);
+    atomicMax(&sh_max, mx);
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        int f = sh_flags;
+        if (carry_tok != T_expected) f |= kDataTokenCount;
+        tok_off[B] = static_cast<int32_t>(carry_tok);
+        att_off[B] = carry_att;
+        status[0] = f;
+        status[1] = 0;
+        status[2] = 0;
+        status[3] = sh_max;
+    }
+}
+
+// rank(b) = #{b' : L_b' > L_b} + #{b' < b : L_b' = L_b}: a strict total order, so
+// `order[rank(b)] = b` writes every slot of order exactly once for any lengths.
+__global__ __launch_bounds__(256) void k_plan_rank(const int32_t* __restrict__ lengths, int B,
+                                                    int32_t* __restrict__ order) {
+    __shared__ int32_t Ls[256];
+    const int b = blockIdx.x * 256 + threadIdx.x;
+    const int Lb = b < B ? lengths[b] : 0;
+    int rank = 0;
+    for (int base = 0; base < B; base += 256) {
+        __syncthreads();
+        Ls[threadIdx.x] = base + threadIdx.x < B ? lengths[base + threadIdx.x] : 0;
+        __syncthreads();
+        const int n = min(256, B - base);
+        for (int k = 0; k < n; ++k) {
+            const int Lk = Ls[k];
+            rank += (Lk > Lb) | ((Lk == Lb) & (base + k < b));
+        }
+    }
+    if (b < B) order[rank] = b;
+}
+
+__global__ __launch_bounds__(kScanThreads) void k_plan_items(const int32_t* __restrict__ lengths,
+                                                              const int32_t* __restrict__ order, int B,
+                                                              int H, int64_t qkt_cap, int64_t av_cap,
+                                                              int32_t* __restrict__ qkt_item_off,
+                                                              int32_t* __restrict__ av_item_off,
+                                                              int32_t* __restrict__ status) {
+    __shared__ int64_t sh_a[kScanWaves], sh_b[kScanWaves];
+    const int flags0 = status[0];
+    int64_t carry_q = 0, carry_a = 0;
+    for (int base = 0; base < B; base += kScanThreads) {
+        const int k = base + threadIdx.x;
+        int64_t nq = 0, na = 0;
+        if (k < B && flags0 == 0) {
+            const int64_t nt = (lengths[order[k]] + kTile - 1) / kTile;
+            na = (int64_t)H * nt;
+            nq = na * nt;
+        }
+        int64_t eq, ea, tq, ta;
+        block_exclusive_scan2(nq, na, eq, ea, tq, ta, sh_a, sh_b);
+        if (k < B) {
+            qkt_item_off[k] = static_cast<int32_t>(min(carry_q + eq, (int64_t)INT_MAX));
+            av_item_off[k] = static_cast<int32_t>(min(carry_a + ea, (int64_t)INT_MAX));
+        }
+        carry_q += tq;
+        carry_a += ta;
+    }
+    if (threadIdx.x == 0) {
+        int f = flags0;
+        if (carry_q > qkt_cap) f |= kDataQktCap;
+        if (carry_a > av_cap) f |= kDataAvCap;
+        qkt_item_off[B] = static_cast<int32_t>(min(carry_q, (int64_t)INT_MAX));
+        av_item_off[B] = static_cast<int32_t>(min(carry_a, (int64_t)INT_MAX));
+        status[0] = f;
+        status[1] = f ? 0 : static_cast<int32_t>(carry_q);
+        status[2] = f ? 0 : static_cast<int32_t>(carry_a);
+    }
+}
+
+// Workgroup k writes the items of the k-th longest sequence and its token map.
+__global__ __launch_bounds__(256) void k_plan_fill(const int32_t* __restrict__ lengths,
+                                                    const int32_t* __restrict__ order,
+                                                    const int32_t* __restrict__ tok_off, int H,
+                                                    const int32_t* __restrict__ qkt_item_off,
+                                                    const int32_t* __restrict__ av_item_off,
+                                                    int32_t* __restrict__ qkt_items,
+                                                    int32_t* __restrict__ av_items,
+                                                    int32_t* __restrict__ tok_seq,
+                                                    const int32_t* __restrict__ status) {
+    if (status[0] != 0) return;
+    const int k = blockIdx.x;
+    const int b = order[k];
+    const int L = lengths[b];
+    const int nt = (L + kTile - 1) / kTile;
+    const int nq = H * nt * nt, na = H * nt;
+    int4* q = reinterpret_cast<int4*>(qkt_items) + qkt_item_off[k];
+    for (int idx = threadIdx.x; idx < nq; idx += 256) {
+        const int h = idx / (nt * nt), r = idx - h * nt * nt;
+        const int ti = r / nt, tj = r - ti * nt;
+        q[idx] = make_int4(b, h, ti, tj);
+    }
+    int32_t* a = av_items + 3 * (int64_t)av_item_off[k];
+    for (int idx = threadIdx.x; idx < na; idx += 256) {
+        const int h = idx / nt, ti = idx - h * nt;
+        a[3 * idx + 0] = b;
+        a[3 * idx + 1] = h;
+        a[3 * idx + 2] = ti;
+    }
+    const int t0 = tok_off[b];
+    for (int t = threadIdx.x; t < L; t += 256) tok_seq[t0 + t] = b;
+}
+
+}  // namespace
+
+hipError_t launch_offsets(const PlanView& p, hipStream_t s) {
+    hipLaunchKernelGGL(k_plan_scan, dim3(1), dim3(kScanThreads), 0, s, p.lengths, p.batch, p.total_tokens,
+                       p.max_len, p.heads, p.tok_off, p.att_off, p.status);
+    hipLaunchKernelGGL(k_plan_rank, dim3((p.batch + 255) / 256), dim3(256), 0, s, p.lengths, p.batch, p.order);
+    hipLaunchKernelGGL(k_plan_items, dim3(1), dim3(kScanThreads), 0, s, p.lengths, p.order, p.batch, p.heads,
+                       p.qkt_cap, p.av_cap, p.qkt_item_off, p.av_item_off, p.status);
+    hipLaunchKernelGGL(k_plan_fill, dim3(p.batch), dim3(256), 0, s, p.lengths, p.order, p.tok_off, p.heads,
+                       p.qkt_item_off, p.av_item_off, p.qkt_items, p.av_items, p.tok_seq, p.status);
+    return hipGetLastError();
+}
+
+}  // namespace rag

@@ -1,0 +1,208 @@
+"""GPU parity of the ragged attention operators against the oracle:
+ragged_qkt, ragged_softmax, ragged_attn_v (fp32 and bf16) and the fused
+ragged_attention (bf16), on the SDPA configurations and on ragged shapes that
+exercise every tile edge, with NaN guard regions around every output."""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from tests.helpers import bf16_close, canary_buffer, canary_intact, close, dev, host, scores_close
+from workloads import make_workload, random_storage
+
+pytestmark = pytest.mark.gpu
+
+
+def _plan(L, H):
+    import paper_2110_10221_amd as rag
+
+    L = np.asarray(L, np.int32)
+    plan = rag.Plan(torch.from_numpy(L).cuda(), int(L.sum()), int(max(L.max(), 1)), H)
+    rag.ragged_offsets(plan)
+    return plan
+
+
+def _run_unfused(L, H, q, k, v, dtype, scale, ld=None):
+    import paper_2110_10221_amd as rag
+
+    T = int(np.sum(L))
+    d = H * 64
+    n = oracle.score_elems(L, H)
+    plan = _plan(L, H)
+    qd, kd, vd = dev(q, dtype), dev(k, dtype), dev(v, dtype)
+    if ld is not None:  # Q, K, V as column blocks of one [T, ld] buffer
+        buf = torch.zeros(T, ld, dtype=qd.dtype, device="cuda")
+        buf[:, :d], buf[:, d:2 * d], buf[:, 2 * d:3 * d] = qd, kd, vd
+        qd, kd, vd = buf[:, :d], buf[:, d:2 * d], buf[:, 2 * d:3 * d]
+    s_whole, S = canary_buffer(n, dtype)
+    p_whole, P = canary_buffer(n, dtype)
+    o_whole, O = canary_buffer(T * d, dtype)
+    rag.ragged_qkt(plan, qd, kd, S, scale)
+    rag.ragged_softmax(plan, S, P)
+    rag.ragged_attn_v(plan, P, vd, O.view(T, d))
+    torch.cuda.synchronize()
+    assert not plan.data_errors(), plan.data_errors()
+    assert canary_intact(s_whole, n) and canary_intact(p_whole, n) and canary_intact(o_whole, T * d)
+    return host(S, dtype), host(P, dtype), host(O, dtype).reshape(T, d)
+
+
+def _oracle_chain(L, H, q, k, v, dtype, scale):
+    d = H * 64
+    S = oracle.qkt(dtype, L, H, 64, q, d, k, d, scale)
+    P = oracle.softmax(dtype, L, H, S)
+    O = oracle.attn_v(dtype, L, H, 64, P, v, d)
+    return S, P, O
+
+
+def _check_ops(L, H, q, k, v, dtype, scale, ld=None, chain=True):
+    """Each operator against the oracle on the same input; with `chain`, also the
+    GPU chain against the oracle chain.  (softmax turns an absolute score error e
+    into a relative probability error e, so in fp32 the chain comparison only
+    holds while |S| * 2^-24 stays well under 1e-5.)"""
+    S, P, O = _run_unfused(L, H, q, k, v, dtype, scale, ld)
+    So, Po, Oo = _oracle_chain(L, H, q, k, v, dtype, scale)
+    assert scores_close(S, So, L, H, dtype), "QK^T"
+    assert scores_close(P, oracle.softmax(dtype, L, H, S), L, H, dtype), "softmax"
+    assert close(O, oracle.attn_v(dtype, L, H, 64, P, v, H * 64), dtype, H * 64), "Attn.V"
+    if chain:
+        assert scores_close(P, Po, L, H, dtype), "softmax (chain)"
+        assert close(O, Oo, dtype, H * 64), "Attn.V (chain)"
+
+
+def test_config1_fp32():
+    wl = make_workload(1, seed=0)
+    print("config 1", wl.lengths.tolist(), flush=True)
+    _check_ops(wl.lengths, wl.cfg.heads, wl.tensors["q"], wl.tensors["k"], wl.tensors["v"], "f32", 0.125)
+
+
+def test_config2_bf16():
+    wl = make_workload(2, seed=0)
+    print("config 2 T =", wl.total_tokens, flush=True)
+    _check_ops(wl.lengths, wl.cfg.heads, wl.tensors["q"], wl.tensors["k"], wl.tensors["v"], "bf16", 0.125)
+
+
+RAGGED = [
+    [1, 15, 16, 17, 63, 64, 65, 127, 129, 200],
+    [0, 7, 0, 300, 2],
+    [513, 40],       # a row longer than the register path of the softmax
+    [64] * 5,
+]
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("L", RAGGED)
+@pytest.mark.parametrize("H", [1, 3])
+def test_ragged_shapes(dtype, L, H):
+    rng = np.random.default_rng(sum(L) * 7 + H)
+    T = sum(L)
+    q, k, v = (random_storage(rng, (T, H * 64), dtype, 0.5) for _ in range(3))
+    _check_ops(np.array(L, np.int32), H, q, k, v, dtype, 1 / 8)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_large_scores_and_strided_qkv(dtype):
+    # N(0, 4^2) inputs with scale 1: peaked rows exercise the max subtraction;
+    # Q, K, V are column blocks of one [T, 3d + 64] buffer
+    rng = np.random.default_rng(3)
+    L, H = np.array([33, 90, 5], np.int32), 2
+    T = int(L.sum())
+    q, k, v = (random_storage(rng, (T, H * 64), dtype, 4.0 if i < 2 else 1.0) for i in range(3))
+    _check_ops(L, H, q, k, v, dtype, 1.0, ld=3 * H * 64 + 64, chain=dtype == "bf16")
+
+
+def test_softmax_in_place_matches_out_of_place():
+    import paper_2110_10221_amd as rag
+
+    rng = np.random.default_rng(4)
+    L, H = np.array([9, 100, 700], np.int32), 2
+    n = oracle.score_elems(L, H)
+    S = dev(random_storage(rng, (n,), "bf16", 3.0), "bf16")
+    plan = _plan(L, H)
+    P = torch.empty_like(S)
+    rag.ragged_softmax(plan, S, P)
+    S2 = S.clone()
+    rag.ragged_softmax(plan, S2)
+    torch.cuda.synchronize()
+    assert torch.equal(P.view(torch.int16), S2.view(torch.int16))
+
+
+def _fused(L, H, q, k, v, scale):
+    import paper_2110_10221_amd as rag
+
+    T = int(np.sum(L))
+    d = H * 64
+    plan = _plan(L, H)
+    o_whole, O = canary_buffer(T * d, "bf16")
+    rag.ragged_attention(plan, dev(q, "bf16"), dev(k, "bf16"), dev(v, "bf16"), O.view(T, d), scale)
+    torch.cuda.synchronize()
+    assert not plan.data_errors()
+    assert canary_intact(o_whole, T * d)
+    return host(O, "bf16").reshape(T, d)
+
+
+@pytest.mark.parametrize("L", RAGGED + [[512] * 3, [8, 64, 9, 384, 511]])
+@pytest.mark.parametrize("H", [1, 4])
+@pytest.mark.parametrize("qk_scale", [0.5, 4.0])
+def test_fused_attention(L, H, qk_scale):
+    rng = np.random.default_rng(sum(L) + H)
+    L = np.array(L, np.int32)
+    T = int(L.sum())
+    if L.max() > 512:  # beyond the fused kernel's register-resident rows: rejected on the host
+        import paper_2110_10221_amd as rag
+
+        plan = _plan(L, H)
+        z = torch.zeros(T, H * 64, dtype=torch.bfloat16, device="cuda")
+        with pytest.raises(rag.RaggedError, match="RAG_ERR_SHAPE"):
+            rag.ragged_attention(plan, z, z, z, torch.empty_like(z), 0.125)
+        return
+    q, k = (random_storage(rng, (T, H * 64), "bf16", qk_scale) for _ in range(2))
+    v = random_storage(rng, (T, H * 64), "bf16", 1.0)
+    got = _fused(L, H, q, k, v, 1 / 8)
+    _, _, ref = _oracle_chain(L, H, q, k, v, "bf16", 1 / 8)
+    ok, worst = bf16_close(got, ref)
+    assert ok, worst
+
+
+def test_fused_attention_config2():
+    wl = make_workload(2, seed=0)
+    L, H = wl.lengths, wl.cfg.heads
+    got = _fused(L, H, wl.tensors["q"], wl.tensors["k"], wl.tensors["v"], 0.125)
+    _, _, ref = _oracle_chain(L, H, wl.tensors["q"], wl.tensors["k"], wl.tensors["v"], "bf16", 0.125)
+    ok, worst = bf16_close(got, ref)
+    assert ok, worst
+
+
+def test_score_buffer_too_small_is_reported_not_written():
+    import paper_2110_10221_amd as rag
+
+    rng = np.random.default_rng(5)
+    L, H = np.array([40, 50], np.int32), 2
+    T = int(L.sum())
+    q = dev(random_storage(rng, (T, 128), "bf16"), "bf16")
+    n = oracle.score_elems(L, H)
+    whole, S = canary_buffer(n - 1, "bf16")
+    plan = _plan(L, H)
+    rag.ragged_qkt(plan, q, q, S, 0.125)
+    torch.cuda.synchronize()
+    assert plan.status[0].item() & 32
+    assert torch.isnan(whole.float()).all()
+
+
+def test_determinism_and_sequence_permutation():
+    rng = np.random.default_rng(6)
+    L, H = np.array([70, 3, 129], np.int32), 2
+    T = int(L.sum())
+    q, k, v = (random_storage(rng, (T, 128), "bf16") for _ in range(3))
+    a = _fused(L, H, q, k, v, 0.125)
+    b = _fused(L, H, q, k, v, 0.125)
+    assert (a == b).all()
+    perm = [2, 0, 1]
+    st = np.concatenate([[0], np.cumsum(L)])
+    cat = lambda x: np.concatenate([x[st[i]:st[i + 1]] for i in perm])
+    c = _fused(L[perm], H, cat(q), cat(k), cat(v), 0.125)
+    assert (c == cat(a)).all()
+    S1, P1, O1 = _run_unfused(L, H, q, k, v, "bf16", 0.125)
+    S2, P2, O2 = _run_unfused(L, H, q, k, v, "bf16", 0.125)
+    assert (S1 == S2).all() and (P1 == P2).all() and (O1 == O2).all()

@@ -1,0 +1,108 @@
+"""GPU parity of encoder_layer against the oracle.
+
+Small layers are compared in full.  At the benchmark sizes (configurations 3-5)
+the GPU runs the whole batch exactly as the benchmark launches it, and the
+oracle recomputes a sample of whole sequences: a sequence's layer output
+depends only on its own tokens (checked on the oracle and below on the GPU), so
+each sampled sequence is an independent oracle case."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from tests.helpers import bf16_close, bf16_row_close, canary_buffer, canary_intact, close, dev, host
+from workloads import WEIGHT_NAMES, BIAS_NAMES, LN_NAMES, make_workload, random_storage
+
+pytestmark = pytest.mark.gpu
+
+
+def _gpu_layer(L, x, w, d, H, dff, dtype, flags=0):
+    import paper_2110_10221_amd as rag
+
+    L = np.asarray(L, np.int32)
+    T = int(L.sum())
+    plan = rag.Plan(torch.from_numpy(L).cuda(), T, int(max(L.max(), 1)), H)
+    rag.ragged_offsets(plan)
+    wd = {n: dev(a, dtype) for n, a in w.items()}
+    code = rag.RAG_F32 if dtype == "f32" else rag.RAG_BF16
+    ws = torch.empty(rag.encoder_layer_workspace(T, int(max(L.max(), 1)), d, H, dff, code, flags),
+                     dtype=torch.uint8, device="cuda")
+    whole, y = canary_buffer(T * d, dtype)
+    rag.encoder_layer(plan, dev(x, dtype), y.view(T, d), wd, dff, ws, flags=flags)
+    torch.cuda.synchronize()
+    assert not plan.data_errors(), plan.data_errors()
+    assert canary_intact(whole, T * d)
+    return host(y, dtype).reshape(T, d)
+
+
+def _small_weights(rng, d, dff, dtype):
+    w = {}
+    for n, shape in (("w_qkv", (3 * d, d)), ("w_o", (d, d)), ("w_ff1", (dff, d)), ("w_ff2", (d, dff))):
+        w[n] = random_storage(rng, shape, dtype, 0.05)
+    for n, m in (("b_qkv", 3 * d), ("b_o", d), ("b_ff1", dff), ("b_ff2", d)):
+        w[n] = random_storage(rng, (m,), dtype, 0.05)
+    for n in LN_NAMES:
+        w[n] = random_storage(rng, (d,), dtype, 0.1)
+    return w
+
+
+@pytest.mark.parametrize("dtype,flags", [("bf16", 0), ("bf16", 1), ("f32", 0)])
+@pytest.mark.parametrize("L", [[5, 70, 33], [1], [0, 64, 0, 129], [200, 17, 64, 3, 99]])
+def test_small_layers(dtype, flags, L):
+    rng = np.random.default_rng(sum(L))
+    L = np.array(L, np.int32)
+    H, d, dff = 2, 128, 256
+    x = random_storage(rng, (int(L.sum()), d), dtype)
+    w = _small_weights(rng, d, dff, dtype)
+    got = _gpu_layer(L, x, w, d, H, dff, dtype, flags)
+    ref = oracle.encoder_layer(dtype, L, x, w, d, H, dff)
+    if dtype == "bf16":
+        ok, worst = bf16_row_close(got, ref, d)
+        assert ok, worst
+    else:
+        assert close(got, ref, "f32", d)
+
+
+def _sample_check(wl, got, picks):
+    cfg = wl.cfg
+    L = wl.lengths
+    st = np.concatenate([[0], np.cumsum(L)])
+    w = {n: wl.tensors[n] for n in WEIGHT_NAMES + BIAS_NAMES + LN_NAMES}
+    for b in picks:
+        print(f"  oracle sequence {b} (L={L[b]})", flush=True)
+        xs = wl.tensors["x"][st[b]:st[b + 1]]
+        ref = oracle.encoder_layer("bf16", L[b:b + 1], xs, w, cfg.d_model, cfg.heads, cfg.d_ff)
+        ok, worst = bf16_row_close(got[st[b]:st[b + 1]], ref, cfg.d_model)
+        elem_ok, elem_worst = bf16_close(got[st[b]:st[b + 1]], ref)
+        print(f"    row-scaled worst excess {worst:.2e}; element-wise worst excess {elem_worst:.2e}", flush=True)
+        assert ok, (b, int(L[b]), worst)
+
+
+@pytest.mark.parametrize("cid,flags", [(3, 0), (3, 1), (5, 0), (4, 0)])
+def test_benchmark_configs_sampled_sequences(cid, flags):
+    wl = make_workload(cid, seed=0, random_ln=True)
+    cfg = wl.cfg
+    print(f"layer config {cid} flags {flags}: B={cfg.batch} T={wl.total_tokens}", flush=True)
+    w = {n: wl.tensors[n] for n in WEIGHT_NAMES + BIAS_NAMES + LN_NAMES}
+    got = _gpu_layer(wl.lengths, wl.tensors["x"], w, cfg.d_model, cfg.heads, cfg.d_ff, "bf16", flags)
+    L = wl.lengths
+    order = np.argsort(-L, kind="stable")
+    # the longest, the shortest and two in between
+    picks = sorted({int(order[0]), int(order[-1]), int(order[len(L) // 2]), int(order[len(L) // 3])})
+    _sample_check(wl, got, picks)
+
+
+def test_layer_permutation_equivariance_and_determinism():
+    wl = make_workload(5, seed=1, random_ln=True)
+    cfg = wl.cfg
+    w = {n: wl.tensors[n] for n in WEIGHT_NAMES + BIAS_NAMES + LN_NAMES}
+    L = wl.lengths
+    a = _gpu_layer(L, wl.tensors["x"], w, cfg.d_model, cfg.heads, cfg.d_ff, "bf16")
+    b = _gpu_layer(L, wl.tensors["x"], w, cfg.d_model, cfg.heads, cfg.d_ff, "bf16")
+    assert (a == b).all()
+    rng = np.random.default_rng(0)
+    perm = rng.permutation(len(L))
+    st = np.concatenate([[0], np.cumsum(L)])
+    cat = lambda arr: np.concatenate([arr[st[i]:st[i + 1]] for i in perm])
+    c = _gpu_layer(L[perm], cat(wl.tensors["x"]), w, cfg.d_model, cfg.heads, cfg.d_ff, "bf16")
+    assert (c == cat(a)).all()
