@@ -17,7 +17,8 @@ import os
 import torch
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "libragged.so")
+# RAG_LIBRARY selects an alternate build of the same library (e.g. a variant)
+LIB_PATH = os.environ.get("RAG_LIBRARY") or os.path.join(_HERE, "libragged.so")
 
 RAG_OK = 0
 RAG_F32, RAG_BF16 = 0, 1

@@ -33,29 +33,37 @@ def hipcc() -> str:
     raise RuntimeError("hipcc not found (ROCm is required to build the HIP library)")
 
 
-def _compile(src: str) -> str:
+def _compile(src: str, defines=(), obj_dir: str = OBJ_DIR) -> str:
     path = os.path.join(CSRC, src)
-    obj = os.path.join(OBJ_DIR, src + ".o")
-    cmd = [hipcc()] + COMMON + (DEVICE if src.endswith(".hip") else []) + ["-c", path, "-o", obj]
+    obj = os.path.join(obj_dir, src + ".o")
+    cmd = [hipcc()] + COMMON + list(defines) + (DEVICE if src.endswith(".hip") else []) + ["-c", path, "-o", obj]
     res = subprocess.run(cmd, capture_output=True, text=True)
     if res.returncode != 0:
         raise RuntimeError(f"compiling {src} failed:\n{' '.join(cmd)}\n{res.stdout}\n{res.stderr}")
     return obj
 
 
-def build(jobs: int | None = None) -> str:
-    os.makedirs(OBJ_DIR, exist_ok=True)
+def build(jobs: int | None = None, out: str = LIB, defines=()) -> str:
+    """Compile and link; `out` and `defines` (extra -D flags) serve alternate builds."""
+    obj_dir = OBJ_DIR if out == LIB else os.path.join(OBJ_DIR, os.path.basename(out) + ".objs")
+    os.makedirs(obj_dir, exist_ok=True)
     jobs = jobs or min(len(SOURCES), os.cpu_count() or 4)
     with concurrent.futures.ThreadPoolExecutor(jobs) as ex:
-        objs = list(ex.map(_compile, SOURCES))
-    tmp = LIB + ".tmp"
+        objs = list(ex.map(lambda src: _compile(src, defines, obj_dir), SOURCES))
+    tmp = out + ".tmp"
     cmd = [hipcc(), "-shared", "-fPIC", f"--offload-arch={ARCH}", "-o", tmp] + objs
     res = subprocess.run(cmd, capture_output=True, text=True)
     if res.returncode != 0:
         raise RuntimeError(f"linking failed:\n{' '.join(cmd)}\n{res.stdout}\n{res.stderr}")
-    os.replace(tmp, LIB)
-    return LIB
+    os.replace(tmp, out)
+    return out
 
 
 if __name__ == "__main__":
-    print(build())
+    import argparse
+
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--out", default=LIB)
+    ap.add_argument("-D", dest="defines", action="append", default=[])
+    a = ap.parse_args()
+    print(build(out=os.path.abspath(a.out), defines=[f"-D{d}" for d in a.defines]))

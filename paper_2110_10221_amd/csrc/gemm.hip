@@ -3,30 +3,95 @@
 // fused loop over the batch and length loops, so they are plain GEMMs with
 // M = T and no padding).
 //
-// bf16: 256x256 output tile per workgroup, K step 64, four waves in a 2x2 grid,
-// each wave a 128x128 sub-tile of v_mfma_f32_16x16x32_bf16 accumulators.  Both
-// operands are K-contiguous in memory (x is [T, K], w is [N, K]), which is the
-// operand layout the MFMA wants, so they are staged through LDS without any
-// transposition.  The MFMA computes the transposed tile C[n][m] = sum_k
-// w[n][k] x[m][k], so each lane ends with four consecutive output features of
-// one token, stored as one 8-byte write with bias / activation / residual fused.
-// LDS rows are 128 bytes; the 16-byte chunk index is XOR-swizzled with the row
-// so that the fragment reads of 16 consecutive rows hit distinct banks.  Two
-// LDS stages: the global loads of step k+1 are in flight while step k computes.
+// bf16: an RAG_GEMM_BM x 256 output tile per workgroup of (BM/128) x 4 waves,
+// each wave a 128 (tokens) x 64 (features) sub-tile of v_mfma_f32_32x32x16_bf16
+// accumulators (the full-rate bf16 MFMA on gfx950).  With BM = 128 a workgroup
+// needs 72 KB of LDS, so two run on each CU and one's prologue / epilogue
+// overlaps the other's K loop.
+//  - Both operands are K-contiguous in memory (x is [T, K], w is [N, K]), the
+//    operand layout the MFMA wants, so tiles go to LDS untransposed.
+//  - Global -> LDS copies are bounds-checked buffer loads that write LDS
+//    directly (no register staging): each wave instruction fills one 1 KB block
+//    of consecutive rows, lane l landing at byte 16*l of the block.  Rows past
+//    T (or N) lie outside the buffer range and arrive as zeros, so the ragged
+//    last token tile needs no clamping.
+//  - The 16-byte chunk index inside an LDS row is XOR-swizzled with the row, so
+//    the fragment reads of consecutive rows spread over the banks; the copies
+//    pick their source chunk so that the swizzled slot is filled.
+//  - Software pipeline over K steps of 32: kStages LDS stages, copies issued
+//    kStages steps ahead; the x fragments of step k+1 are read into a second
+//    register set right after the barrier and its w fragments are streamed in
+//    while the MFMAs of step k run.  The barrier waits only for the copies the
+//    next step needs.
+//  - The MFMA computes the transposed tile C[n][m] = sum_k w[n][k] x[m][k], so each
+//    lane ends with four consecutive output features of one token.  The fp32
+//    results pass through LDS in 32-token slices so that bias / activation /
+//    residual are applied while whole 512-byte rows move to and from memory.
+#include <type_traits>
+
 #include "device_common.h"
 #include "launch.h"
 
 namespace rag {
 namespace {
 
-constexpr int BM = 256, BN = 256, BK = 64;
-constexpr int kGemmThreads = 256;
-constexpr int WM = 128, WN = 128;           // wave tile
-constexpr int FM = WM / 16, FN = WN / 16;   // 16x16 fragments per wave
-constexpr int kRowsPerPass = kGemmThreads / 8;  // 8 chunks of 16 B per 128-B row
-constexpr int kPasses = BM / kRowsPerPass;      // 8
+typedef __attribute__((address_space(3))) void lds_void_t;
 
-__device__ __forceinline__ int swz(int row, int chunk) { return (chunk ^ (row & 7)); }
+#ifndef RAG_GEMM_BM
+#define RAG_GEMM_BM 128
+#endif
+#ifndef RAG_GEMM_STAGES
+#define RAG_GEMM_STAGES 3
+#endif
+constexpr int BM = RAG_GEMM_BM, BN = 256, BK = 32;
+constexpr int kStages = RAG_GEMM_STAGES;
+constexpr int kWavesM = BM / 128, kWavesN = 4;
+constexpr int kGemmWaves = kWavesM * kWavesN, kGemmThreads = kGemmWaves * kWave;
+constexpr int WM = 128, WN = 64;            // wave tile (tokens x features)
+constexpr int FM = WM / 32, FN = WN / 32;   // 32x32 fragments per wave
+constexpr int KSTEPS = BK / 16;             // MFMA k-steps per K step
+constexpr int kChunks = BK / 8;             // 16-byte chunks per LDS row
+constexpr int kRowsPerBlock = 64 / kChunks; // rows filled by one 1 KB wave copy
+constexpr int kStageElems = (BM + BN) * BK; // one LDS stage: x tile then w tile
+constexpr int kXBlocksPerWave = BM / kRowsPerBlock / kGemmWaves;  // 1 KB blocks of x per wave
+constexpr int kWBlocksPerWave = BN / kRowsPerBlock / kGemmWaves;  // 1 KB blocks of w per wave
+constexpr int kCopiesPerStep = kXBlocksPerWave + kWBlocksPerWave;  // copy instructions per wave per K step
+constexpr int kEpiRows = 32;                                       // tokens per epilogue slice
+constexpr int kEpilogueBytes = kEpiRows * BN * 4;
+constexpr int kLdsBytes = kStages * kStageElems * 2 > kEpilogueBytes ? kStages * kStageElems * 2 : kEpilogueBytes;
+static_assert(kStages >= 2 && kLdsBytes <= 160 * 1024, "LDS budget");
+static_assert(kXBlocksPerWave >= 1 && kWBlocksPerWave >= 1, "copy split");
+
+__device__ __forceinline__ int swz(int row) { return (row >> 1) & (kChunks - 1); }
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, bytes, 0x00020000);
+}
+
+// Per-lane byte offset for copying a block of kRowsPerBlock rows starting at
+// row0: lane l fills LDS slot l (row row0 + l / kChunks, physical chunk
+// l % kChunks) and so reads the logical chunk that the swizzle maps there.
+__device__ __forceinline__ int copy_voffset(int lane, int row0, int ld_bytes) {
+    const int row = row0 + lane / kChunks;
+    return row * ld_bytes + ((lane % kChunks) ^ swz(row)) * 16;
+}
+
+// One wave fills the 1 KB LDS block `dst`; k0b (the K offset in bytes) is
+// wave-uniform and travels in the scalar offset.
+__device__ __forceinline__ void copy_block(__amdgpu_buffer_rsrc_t rsrc, uint16_t* dst, int voff, int k0b) {
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, (lds_void_t*)dst, 16, voff, k0b, 0, 0);
+}
+
+// Workgroup barrier that waits for LDS traffic but not for the copies still in
+// flight (a __syncthreads() fence would drain them all): the caller has already
+// waited for the copies it needs.
+__device__ __forceinline__ void barrier_lds() {
+    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
+__device__ __forceinline__ bf16x8 lds_frag(const uint16_t* tile, int row, int chunk) {
+    return as_bf16x8(*reinterpret_cast<const u32x4*>(tile + row * BK + ((chunk ^ swz(row)) * 8)));
+}
 
 // Map the linear workgroup id so that each XCD (workgroups are dealt to the 8
 // XCDs round-robin) receives a contiguous range of output tiles.
@@ -36,116 +101,165 @@ __device__ __forceinline__ int xcd_remap(int bid, int nblocks) {
     return xcd < rem ? xcd * (per + 1) + idx : rem * (per + 1) + (xcd - rem) * per + idx;
 }
 
+// Wait until at most `n` copy instructions of this wave are outstanding (the
+// copies complete in issue order).
+__device__ __forceinline__ void wait_copies(int n) {
+    if (n >= 3 * kCopiesPerStep) asm volatile("s_waitcnt vmcnt(%0)" ::"n"(3 * kCopiesPerStep) : "memory");
+    else if (n >= 2 * kCopiesPerStep) asm volatile("s_waitcnt vmcnt(%0)" ::"n"(2 * kCopiesPerStep) : "memory");
+    else if (n >= kCopiesPerStep) asm volatile("s_waitcnt vmcnt(%0)" ::"n"(kCopiesPerStep) : "memory");
+    else asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+}
+
 template <int ACT, bool HAS_BIAS, bool HAS_RES>
-__global__ __launch_bounds__(kGemmThreads) __attribute__((amdgpu_waves_per_eu(1, 1)))
+__global__ __launch_bounds__(kGemmThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void k_gemm_bf16(const uint16_t* __restrict__ x, int ldx, const uint16_t* __restrict__ w,
                  const uint16_t* __restrict__ bias, const uint16_t* residual, int ldr, uint16_t* y, int ldy,
                  int T, int K, int N, int tiles_n) {
     extern __shared__ __attribute__((aligned(16))) uint16_t smem[];
-    // stage s: x tile at smem + s*BM*BK, w tile at smem + 2*BM*BK + s*BN*BK
-
     const int tile = xcd_remap(blockIdx.x, gridDim.x);
     const int tm = tile / tiles_n, tn = tile % tiles_n;
     const int m0 = tm * BM, n0 = tn * BN;
-    const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
-    const int wm = wave / 2, wn = wave % 2;
-    const int l16 = lane % 16, q4 = lane / 16;
+    const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
+    const int wm = wave / kWavesN, wn = wave % kWavesN;
+    const int l32 = lane % 32, h2 = lane / 32;
 
-    // global -> register staging: thread loads chunk (tid & 7) of rows (tid >> 3) + 32 * p
-    const int ld_chunk = tid & 7, ld_row = tid >> 3;
-    const uint16_t* xg[kPasses];
-    const uint16_t* wg[kPasses];
+    const __amdgpu_buffer_rsrc_t rx = make_rsrc(x + (int64_t)m0 * ldx, (uint32_t)min(T - m0, BM) * ldx * 2u);
+    const __amdgpu_buffer_rsrc_t rw = make_rsrc(w + (int64_t)n0 * K, (uint32_t)min(N - n0, BN) * K * 2u);
+    int vx[kXBlocksPerWave], vw[kWBlocksPerWave];
 #pragma unroll
-    for (int p = 0; p < kPasses; ++p) {
-        const int r = ld_row + kRowsPerPass * p;
-        xg[p] = x + (int64_t)min(m0 + r, T - 1) * ldx + ld_chunk * 8;
-        wg[p] = w + (int64_t)min(n0 + r, N - 1) * K + ld_chunk * 8;
-    }
-    u32x4 xr[kPasses], wr[kPasses];
-    auto load_global = [&](int k0) {
+    for (int i = 0; i < kXBlocksPerWave; ++i)
+        vx[i] = copy_voffset(lane, (wave * kXBlocksPerWave + i) * kRowsPerBlock, ldx * 2);
 #pragma unroll
-        for (int p = 0; p < kPasses; ++p) {
-            xr[p] = *reinterpret_cast<const u32x4*>(xg[p] + k0);
-            wr[p] = *reinterpret_cast<const u32x4*>(wg[p] + k0);
-        }
-    };
-    auto store_lds = [&](int buf) {
+    for (int i = 0; i < kWBlocksPerWave; ++i)
+        vw[i] = copy_voffset(lane, (wave * kWBlocksPerWave + i) * kRowsPerBlock, K * 2);
+    auto issue = [&](int step) {
+        uint16_t* xs = smem + (step % kStages) * kStageElems;
+        uint16_t* ws = xs + BM * BK;
+        const int k0b = step * BK * 2;
 #pragma unroll
-        for (int p = 0; p < kPasses; ++p) {
-            const int r = ld_row + kRowsPerPass * p;
-            *reinterpret_cast<u32x4*>(smem + buf * BM * BK + r * BK + swz(r, ld_chunk) * 8) = xr[p];
-            *reinterpret_cast<u32x4*>(smem + 2 * BM * BK + buf * BN * BK + r * BK + swz(r, ld_chunk) * 8) = wr[p];
-        }
+        for (int i = 0; i < kXBlocksPerWave; ++i) copy_block(rx, xs + (wave * kXBlocksPerWave + i) * 512, vx[i], k0b);
+#pragma unroll
+        for (int i = 0; i < kWBlocksPerWave; ++i) copy_block(rw, ws + (wave * kWBlocksPerWave + i) * 512, vw[i], k0b);
     };
 
-    floatx4 acc[FN][FM];
+    floatx16 acc[FN][FM];
 #pragma unroll
     for (int i = 0; i < FN; ++i)
 #pragma unroll
-        for (int j = 0; j < FM; ++j) acc[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
-
-    const int nk = K / BK;
-    load_global(0);
-    store_lds(0);
-    __syncthreads();
-    for (int kt = 0; kt < nk; ++kt) {
-        const int cur = kt & 1;
-        if (kt + 1 < nk) load_global((kt + 1) * BK);
-        const uint16_t* xb = smem + cur * BM * BK;
-        const uint16_t* wb = smem + 2 * BM * BK + cur * BN * BK;
+        for (int j = 0; j < FM; ++j)
 #pragma unroll
-        for (int ks = 0; ks < BK / 32; ++ks) {
-            const int chunk = ks * 4 + q4;
-            bf16x8 af[FN], bfr[FM];
+            for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+
+    // Fragments of one K step: fa[ks][i] (w rows), fb[ks][j] (x rows).
+    bf16x8 fa0[KSTEPS][FN], fb0[KSTEPS][FM], fa1[KSTEPS][FN], fb1[KSTEPS][FM];
+    auto read_x = [&](bf16x8 (&fb)[KSTEPS][FM], int step) {
+        const uint16_t* xb = smem + (step % kStages) * kStageElems;
+#pragma unroll
+        for (int ks = 0; ks < KSTEPS; ++ks)
+#pragma unroll
+            for (int j = 0; j < FM; ++j) fb[ks][j] = lds_frag(xb, wm * WM + j * 32 + l32, ks * 2 + h2);
+    };
+    auto read_w1 = [&](bf16x8 (&fa)[KSTEPS][FN], int step, int ks, int i) {
+        const uint16_t* wb = smem + (step % kStages) * kStageElems + BM * BK;
+        fa[ks][i] = lds_frag(wb, wn * WN + i * 32 + l32, ks * 2 + h2);
+    };
+    // one K step with a successor: prefetch its fragments while the MFMAs run
+    auto step_next = [&](bf16x8 (&fa)[KSTEPS][FN], bf16x8 (&fb)[KSTEPS][FM], bf16x8 (&na)[KSTEPS][FN],
+                         bf16x8 (&nb)[KSTEPS][FM], int kt, int nk) {
+        wait_copies(min(kStages - 2, nk - 2 - kt) * kCopiesPerStep);
+        barrier_lds();  // step kt+1's stage is visible; step kt's stage is no longer read
+        if (kt + kStages < nk) issue(kt + kStages);
+        read_x(nb, kt + 1);
+#pragma unroll
+        for (int ks = 0; ks < KSTEPS; ++ks)
 #pragma unroll
             for (int i = 0; i < FN; ++i) {
-                const int r = wn * WN + i * 16 + l16;
-                af[i] = as_bf16x8(*reinterpret_cast<const u32x4*>(wb + r * BK + swz(r, chunk) * 8));
-            }
 #pragma unroll
-            for (int j = 0; j < FM; ++j) {
-                const int r = wm * WM + j * 16 + l16;
-                bfr[j] = as_bf16x8(*reinterpret_cast<const u32x4*>(xb + r * BK + swz(r, chunk) * 8));
+                for (int j = 0; j < FM; ++j) acc[i][j] = mfma32x32x16(fa[ks][i], fb[ks][j], acc[i][j]);
+                read_w1(na, kt + 1, ks, i);
             }
+    };
+    auto step_last = [&](bf16x8 (&fa)[KSTEPS][FN], bf16x8 (&fb)[KSTEPS][FM]) {
+#pragma unroll
+        for (int ks = 0; ks < KSTEPS; ++ks)
 #pragma unroll
             for (int i = 0; i < FN; ++i)
 #pragma unroll
-                for (int j = 0; j < FM; ++j) acc[i][j] = mfma16x16x32(af[i], bfr[j], acc[i][j]);
-        }
-        if (kt + 1 < nk) store_lds(cur ^ 1);
-        __syncthreads();
-    }
+                for (int j = 0; j < FM; ++j) acc[i][j] = mfma32x32x16(fa[ks][i], fb[ks][j], acc[i][j]);
+    };
 
-    // epilogue: acc[i][j][r] = y[m][n + r], m = m0 + wm*128 + j*16 + l16,
-    // n = n0 + wn*128 + i*16 + 4*q4
+    const int nk = K / BK;
 #pragma unroll
-    for (int i = 0; i < FN; ++i) {
-        const int n = n0 + wn * WN + i * 16 + 4 * q4;
-        if (n >= N) continue;
-        float bv[4] = {0.f, 0.f, 0.f, 0.f};
-        if constexpr (HAS_BIAS) {
-            const u32x2 bb = *reinterpret_cast<const u32x2*>(bias + n);
+    for (int st = 0; st < kStages; ++st)
+        if (st < nk) issue(st);
+    wait_copies(min(kStages - 1, nk - 1) * kCopiesPerStep);
+    barrier_lds();
+    read_x(fb0, 0);
+#pragma unroll
+    for (int ks = 0; ks < KSTEPS; ++ks)
+#pragma unroll
+        for (int i = 0; i < FN; ++i) read_w1(fa0, 0, ks, i);
+    // K is a multiple of 64, so nk = K / 32 is even: steps pair up with one exit path
+    for (int kt = 0; kt + 2 < nk; kt += 2) {
+        step_next(fa0, fb0, fa1, fb1, kt, nk);
+        step_next(fa1, fb1, fa0, fb0, kt + 1, nk);
+    }
+    step_next(fa0, fb0, fa1, fb1, nk - 2, nk);
+    step_last(fa1, fb1);
+
+    // Epilogue through LDS, 32 tokens at a time: the wave holding a slice writes
+    // its fp32 accumulators there, then all waves read whole rows back (16 bytes
+    // per lane, 256 features per row), apply bias, activation and residual and
+    // store 512-byte rows.  acc[i][j][4g + r] holds (token j*32 + l32, feature
+    // i*32 + 8g + 4*h2 + r) of the wave's sub-tile.  LDS layout: row r of 64
+    // 16-byte chunks, chunk c at physical slot c ^ r.
+    float* ep = reinterpret_cast<float*>(smem);
+    const int ncol = n0 + 4 * lane;  // this lane's four output features in the row phase
+    float bv[4] = {0.f, 0.f, 0.f, 0.f};
+    if constexpr (HAS_BIAS) {
+        if (ncol < N) {
+            const u32x2 bb = *reinterpret_cast<const u32x2*>(bias + ncol);
             bv[0] = lo_bf16(bb[0]);
             bv[1] = hi_bf16(bb[0]);
             bv[2] = lo_bf16(bb[1]);
             bv[3] = hi_bf16(bb[1]);
         }
+    }
+    constexpr int kRowsPerWave = kEpiRows / kGemmWaves;
 #pragma unroll
-        for (int j = 0; j < FM; ++j) {
-            const int m = m0 + wm * WM + j * 16 + l16;
-            if (m >= T) continue;
-            float o[4];
+    for (int slice = 0; slice < BM / kEpiRows; ++slice) {
+        barrier_lds();  // the K loop (first slice) or the previous slice is done with LDS
+        if (wm == slice / FM) {
 #pragma unroll
-            for (int r = 0; r < 4; ++r) o[r] = activate<ACT>(acc[i][j][r] + bv[r]);
-            if constexpr (HAS_RES) {
-                const u32x2 rr = *reinterpret_cast<const u32x2*>(residual + (int64_t)m * ldr + n);
-                o[0] += lo_bf16(rr[0]);
-                o[1] += hi_bf16(rr[0]);
-                o[2] += lo_bf16(rr[1]);
-                o[3] += hi_bf16(rr[1]);
+            for (int i = 0; i < FN; ++i)
+#pragma unroll
+                for (int g = 0; g < 4; ++g) {
+                    const int c = (wn * WN + i * 32 + 8 * g + 4 * h2) >> 2;
+                    const floatx16& a = acc[i][slice % FM];
+                    const floatx4 o = {a[4 * g], a[4 * g + 1], a[4 * g + 2], a[4 * g + 3]};
+                    *reinterpret_cast<floatx4*>(ep + (l32 * 64 + (c ^ l32)) * 4) = o;
+                }
+        }
+        barrier_lds();
+#pragma unroll
+        for (int rr = 0; rr < kRowsPerWave; ++rr) {
+            const int r = wave * kRowsPerWave + rr;
+            const int m = m0 + slice * kEpiRows + r;
+            if (m < T && ncol < N) {
+                const floatx4 o = *reinterpret_cast<const floatx4*>(ep + (r * 64 + (lane ^ r)) * 4);
+                float v[4];
+#pragma unroll
+                for (int e = 0; e < 4; ++e) v[e] = activate_bf16<ACT>(o[e] + bv[e]);
+                if constexpr (HAS_RES) {
+                    const u32x2 rv = *reinterpret_cast<const u32x2*>(residual + (int64_t)m * ldr + ncol);
+                    v[0] += lo_bf16(rv[0]);
+                    v[1] += hi_bf16(rv[0]);
+                    v[2] += lo_bf16(rv[1]);
+                    v[3] += hi_bf16(rv[1]);
+                }
+                *reinterpret_cast<u32x2*>(y + (int64_t)m * ldy + ncol) =
+                    u32x2{pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3])};
             }
-            const u32x2 out = {pack_bf16x2(o[0], o[1]), pack_bf16x2(o[2], o[3])};
-            *reinterpret_cast<u32x2*>(y + (int64_t)m * ldy + n) = out;
         }
     }
 }
@@ -202,7 +316,7 @@ template <int ACT, bool HB, bool HR>
 hipError_t launch_bf16_variant(const void* x, int ldx, const void* w, const void* bias, const void* residual,
                                int ldr, void* y, int ldy, int T, int K, int N, hipStream_t s) {
     const int tiles_m = (T + BM - 1) / BM, tiles_n = (N + BN - 1) / BN;
-    const size_t lds = 2 * (BM + BN) * BK * sizeof(uint16_t);
+    const size_t lds = kLdsBytes;
     static bool attr_set = false;  // benign race: every thread sets the same value
     if (!attr_set) {
         hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_gemm_bf16<ACT, HB, HR>),
