@@ -149,6 +149,50 @@ def cpu_baseline(wl, target_flops):
             "ms_per_layer_extrapolated": round(useful_flops(L, cfg.d_model, cfg.d_ff) / (fl / dt) * 1e3, 1)}
 
 
+def _counter_per_dispatch(path, counter):
+    """kernel name -> mean counter value per dispatch (KiB for FETCH_SIZE / WRITE_SIZE)."""
+    import csv
+    import collections
+
+    tot, cnt = collections.defaultdict(float), collections.defaultdict(int)
+    with open(path) as f:
+        for r in csv.DictReader(f):
+            if r["Counter_Name"] != counter:
+                continue
+            tot[r["Kernel_Name"]] += float(r["Counter_Value"])
+            cnt[r["Kernel_Name"]] += 1
+    return {k: tot[k] / cnt[k] for k in tot}
+
+
+def _short(name):
+    """Demangled kernel name -> 'k_name<args>' as used in STAGE_KERNEL."""
+    base = name.replace("rag::(anonymous namespace)::", "").replace("void ", "", 1)
+    return base.split("(")[0].strip()
+
+
+def derive_traffic(fetch_csv, write_csv, cal_fetch_csv, cal_write_csv, copy_mib):
+    """HBM bytes per launch of every library kernel: FETCH_SIZE + WRITE_SIZE (KiB per
+    dispatch), each scaled by copy_bytes / counter for a plain copy of known size."""
+    fetch, write = _counter_per_dispatch(fetch_csv, "FETCH_SIZE"), _counter_per_dispatch(write_csv, "WRITE_SIZE")
+    cf, cw = _counter_per_dispatch(cal_fetch_csv, "FETCH_SIZE"), _counter_per_dispatch(cal_write_csv, "WRITE_SIZE")
+    big = lambda d: max(d.values())  # the copy kernel is the dispatch with the largest counts
+    copy_kib = copy_mib * 1024.0
+    sf, sw = copy_kib / big(cf), copy_kib / big(cw)
+    out = {"_calibration": {"copy_mib": copy_mib, "fetch_scale": sf, "write_scale": sw,
+                            "copy_fetch_kib": big(cf), "copy_write_kib": big(cw)}}
+    for k in fetch:
+        short = _short(k)
+        src = KERNEL_SOURCES.get(short.split("<")[0])
+        if src is None:
+            continue
+        out[short] = {"bytes_per_launch": round((fetch[k] * sf + write.get(k, 0.0) * sw) * 1024.0),
+                      "fetch_kib_raw": fetch[k], "write_kib_raw": write.get(k), "source_sha": source_hash(src)}
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    with open(path, "w") as f:
+        json.dump(out, f, indent=1, sort_keys=True)
+    print(json.dumps(out, indent=1, sort_keys=True))
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -159,7 +203,27 @@ def main():
     ap.add_argument("--flags", type=int, default=0, help="encoder_layer flags (1 = unfused attention)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-target-flops", type=float, default=2.0e10)
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
+                    help="only run a plain device copy of MIB MiB five times (counter calibration) and exit")
+    ap.add_argument("--derive-traffic", nargs=4, metavar=("FETCH_CSV", "WRITE_CSV", "CAL_FETCH_CSV", "CAL_WRITE_CSV"),
+                    help="turn rocprofv3 --pmc FETCH_SIZE / WRITE_SIZE counter files of a bench run and of a "
+                         "copy-calibration run into profiles/traffic.json, then exit")
+    ap.add_argument("--copy-mib", type=int, default=512, help="size of the calibration copy (for --derive-traffic)")
     args = ap.parse_args()
+    if args.derive_traffic:
+        derive_traffic(*args.derive_traffic, copy_mib=args.copy_mib)
+        return
+    if args.copy_calibration:
+        import torch
+
+        n = args.copy_calibration * (1 << 20) // 4
+        src = torch.ones(n, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(5):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_calibration_mib": args.copy_calibration, "repeats": 5}))
+        return
     if args.gpus != 1:
         print(f"bench.py runs on exactly one GPU; --gpus {args.gpus} is not supported "
               "(the build targets a single MI355X; sharding is a design note only)", file=sys.stderr)

@@ -12,6 +12,7 @@
 // bf16 kernels use v_mfma_f32_16x16x32_bf16.  In a 16x16x32 MFMA lane l supplies
 // row (l % 16) of A and column (l % 16) of B, each with the 8 consecutive k values
 // 8*(l/16) .. 8*(l/16)+7, and receives C rows 4*(l/16) .. 4*(l/16)+3 of column l % 16.
+#include <algorithm>
 #include <cfloat>
 
 #include "device_common.h"
@@ -359,167 +360,174 @@ __global__ __launch_bounds__(256) void k_attn_v_f32(PlanArgs pa, const float* __
 
 
 // ---------------------------------------------------------------------------
-// Fused ragged attention: QK^T, softmax and Attn.V of one item (sequence b,
-// head h, 64 query rows) in one workgroup, with the same rounding points as the
-// three separate operators: scores rounded to bf16, an exact two-pass softmax
-// (row max and row sum over all of the sequence's keys first), probabilities
-// rounded to bf16, fp32 accumulation of P.V.  Each wave owns 16 query rows and
-// keeps their bf16 scores packed in registers (up to kFusedMaxTiles key tiles,
-// i.e. rows of up to 512 keys), so the H * sum L_b^2 scores never reach memory.
-//   pass 1  stream the sequence's K tiles:   S^T tile C[j][i] = sum_c K[j][c] Q[i][c];
-//           lane holds row i = lane % 16, keys j = jb*16 + 4*(lane/16) + r
-//   pass 2  stream the V tiles:               O^T C[c][i] = sum_j V[j][c] P[i][j]
-//           with P straight from registers: the MFMA pairs the k-th element of A
-//           with the k-th element of B, so the lane's keys {4q..4q+3, 16+4q..16+4q+3}
-//           of each 32-key step serve as its 8 k values and the V operand is read
-//           for the same keys.
-// K tiles sit in LDS as [j][c] (16-byte chunks XOR-swizzled by row), V tiles
-// transposed as [c][j]; both double-buffered, the next tile's global loads in
-// flight while the current one is used.
+// Fused ragged attention: QK^T, softmax and Attn.V of one (sequence b, head h)
+// pair per workgroup of eight waves, with the same rounding points as the
+// three separate operators: scores rounded to bf16, an exact softmax over the
+// whole row, probabilities rounded to bf16, fp32 accumulation of P.V.  No
+// score reaches memory.
+//   load    the pair's K and V rows (at most RAG_FUSED_MAX_LEN of them) are
+//           copied once into LDS with bounds-checked buffer loads that write
+//           LDS directly (16-byte chunks XOR-swizzled by row)
+//   then each wave takes 32-query blocks of the sequence in turn:
+//   pass 1  S^T = K Q^T per 32 keys with v_mfma_f32_32x32x16_bf16 (lane holds
+//           query i = lane % 32 and keys 8*(r/4) + 4*(lane/32) + r%4), round to
+//           bf16, keep the running row maximum and the running sum of
+//           exp(s - max) (rescaled when the maximum grows)
+//   pass 2  recompute the same bf16 scores, form p = bf16(exp(s - max) / sum)
+//           and accumulate O^T = V^T P^T.  The lane's eight keys of each 16-key
+//           step {4h..4h+3, 8+4h..8+4h+3} (h = lane/32) are its k values (the
+//           MFMA pairs the k-th element of A with the k-th element of B), and
+//           ds_read_b64_tr_b16 gathers the V operand for exactly those keys
+//           from the row-major V rows.
+// Pairs are taken longest sequence first (the plan's order), so the largest
+// blocks of work start first.  Recomputing the scores costs one extra QK^T but
+// keeps the registers low enough for two waves per SIMD.
 // ---------------------------------------------------------------------------
 
-constexpr int kFusedMaxTiles = 8;  // longest supported sequence: 8 * 64 = 512 keys
+typedef __attribute__((address_space(3))) void lds_void_t;
+typedef __attribute__((ext_vector_type(4))) short short4_t;
+typedef __attribute__((address_space(3))) short4_t lds_short4_t;
+
+constexpr int kAttnWaves = 8, kAttnThreads = kAttnWaves * kWave;
+constexpr int kAttnMaxLen = 512;                         // RAG_FUSED_MAX_LEN
+constexpr int kAttnKVElems = kAttnMaxLen * kHeadDim;      // one of K or V in LDS
+constexpr size_t kAttnLds = 2 * kAttnKVElems * sizeof(uint16_t);
 
 __device__ __forceinline__ float bf16_round(float x) { return bf16_to_f32(f32_to_bf16(x)); }
 
-struct Row16 {
-    u32x4 a, b;
-};
+// Element offset of (row, col) in [rows][64 channels] LDS storage whose 16-byte
+// chunks are XOR-swizzled by the row.
+__device__ __forceinline__ int kv_off(int row, int col) { return row * kHeadDim + ((((col >> 3) ^ row) & 7) << 3) + (col & 7); }
 
-// 16 channels (starting at column `col`) of key row j of a sequence starting at
-// token t0; rows past the sequence read its last row and come back as zeros.
-__device__ __forceinline__ Row16 fetch_row16(const uint16_t* base, int ld, int t0, int j, int L, int col) {
-    const uint16_t* p = base + (int64_t)(t0 + min(j, L - 1)) * ld + col;
-    Row16 r{ld16(p), ld16(p + 8)};
-    if (j >= L) r.a = r.b = u32x4{0u, 0u, 0u, 0u};
-    return r;
-}
+__device__ __forceinline__ void attn_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
 
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k_attention_bf16(PlanArgs pa, const uint16_t* __restrict__ q, int ldq,
-                                                         const uint16_t* __restrict__ k, int ldk,
-                                                         const uint16_t* __restrict__ v, int ldv, float scale,
-                                                         uint16_t* __restrict__ O, int ldo) {
+__global__ __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
+void k_attention_bf16(PlanArgs pa, const int32_t* __restrict__ order, const uint16_t* __restrict__ q, int ldq,
+                      const uint16_t* __restrict__ k, int ldk, const uint16_t* __restrict__ v, int ldv, float scale,
+                      uint16_t* __restrict__ O, int ldo) {
     if (pa.status[0] != 0) return;
-    __shared__ __attribute__((aligned(16))) uint16_t Ks[2][kTile * kHeadDim];
-    __shared__ __attribute__((aligned(16))) uint16_t Vt[2][kHeadDim][kStage];
-    const int n_items = pa.status[2];
+    extern __shared__ __attribute__((aligned(16))) uint16_t kvs[];  // K rows, then V rows
+    const int H = pa.heads;
+    const int n_pairs = pa.batch * H;
     const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
-    const int l16 = lane % 16, q4 = lane / 16;
-    const int ld_row = threadIdx.x >> 2, ld_c = (threadIdx.x & 3) * 16;  // loader: 16 channels of one key
-    for (int it = blockIdx.x; it < n_items; it += gridDim.x) {
-        const int b = pa.av_items[3 * it], h = pa.av_items[3 * it + 1], ti = pa.av_items[3 * it + 2];
+    const int l32 = lane % 32, h2 = lane / 32;
+    // transposed-read addressing inside a 16-lane group (see the header comment)
+    const int tr_e = (lane % 16) / 4, tr_q = lane % 4, tr_g = lane / 16;
+
+    for (int pair = blockIdx.x; pair < n_pairs; pair += gridDim.x) {
+        const int b = order[pair / H], h = pair % H;
         const int L = pa.lengths[b];
+        if (L == 0) continue;
         const int t0 = pa.tok_off[b];
-        const int nkt = (L + kTile - 1) / kTile;
-        const int qi = min(ti * kTile + wave * 16 + l16, L - 1);
-        const uint16_t* qrow = q + (int64_t)(t0 + qi) * ldq + h * kHeadDim + 8 * q4;
-        const bf16x8 qa0 = as_bf16x8(ld16(qrow)), qa1 = as_bf16x8(ld16(qrow + 32));
-
-        Row16 rw;  // one key's 16 channels in flight (K in pass 1, V in pass 2)
-        auto store_k = [&](int buf) {
-            const int c0 = ld_c / 8;
-            *reinterpret_cast<u32x4*>(&Ks[buf][ld_row * kHeadDim + ((c0 ^ (ld_row & 7)) * 8)]) = rw.a;
-            *reinterpret_cast<u32x4*>(&Ks[buf][ld_row * kHeadDim + (((c0 + 1) ^ (ld_row & 7)) * 8)]) = rw.b;
-        };
-        auto store_v = [&](int buf) {
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                Vt[buf][ld_c + 2 * e][ld_row] = static_cast<uint16_t>(rw.a[e] & 0xffffu);
-                Vt[buf][ld_c + 2 * e + 1][ld_row] = static_cast<uint16_t>(rw.a[e] >> 16);
-                Vt[buf][ld_c + 8 + 2 * e][ld_row] = static_cast<uint16_t>(rw.b[e] & 0xffffu);
-                Vt[buf][ld_c + 8 + 2 * e + 1][ld_row] = static_cast<uint16_t>(rw.b[e] >> 16);
-            }
-        };
-
-        // ---- pass 1: bf16 scores of this wave's 16 rows, packed in registers
-        uint32_t sp[kFusedMaxTiles][8];  // [tile][jb*2 + pair]: keys jb*16 + 4*q4 + {0,1} / {2,3}
-        float mrow = -INFINITY;
-        rw = fetch_row16(k, ldk, t0, ld_row, L, h * kHeadDim + ld_c);
-        __syncthreads();  // the previous item is done with the LDS buffers
-        store_k(0);
-        __syncthreads();
-#pragma unroll
-        for (int kt = 0; kt < kFusedMaxTiles; ++kt) {
-            if (kt < nkt) {
-                const int cur = kt & 1;
-                if (kt + 1 < nkt) rw = fetch_row16(k, ldk, t0, (kt + 1) * kTile + ld_row, L, h * kHeadDim + ld_c);
-#pragma unroll
-                for (int jb = 0; jb < 4; ++jb) {
-                    const int r = jb * 16 + l16;
-                    const bf16x8 k0 = as_bf16x8(*reinterpret_cast<const u32x4*>(&Ks[cur][r * kHeadDim + ((q4 ^ (r & 7)) * 8)]));
-                    const bf16x8 k1 =
-                        as_bf16x8(*reinterpret_cast<const u32x4*>(&Ks[cur][r * kHeadDim + (((4 + q4) ^ (r & 7)) * 8)]));
-                    floatx4 st = {0.f, 0.f, 0.f, 0.f};
-                    st = mfma16x16x32(k0, qa0, st);
-                    st = mfma16x16x32(k1, qa1, st);
-                    float sv[4];
-#pragma unroll
-                    for (int rr = 0; rr < 4; ++rr) {
-                        const int j = kt * kTile + jb * 16 + 4 * q4 + rr;
-                        sv[rr] = j < L ? bf16_round(st[rr] * scale) : -INFINITY;
-                        mrow = fmaxf(mrow, sv[rr]);
-                    }
-                    sp[kt][jb * 2] = pack_bf16x2(sv[0], sv[1]);
-                    sp[kt][jb * 2 + 1] = pack_bf16x2(sv[2], sv[3]);
-                }
-                if (kt + 1 < nkt) store_k(cur ^ 1);
-                __syncthreads();
-            }
+        const __amdgpu_buffer_rsrc_t rk = __builtin_amdgcn_make_buffer_rsrc(
+            const_cast<uint16_t*>(k + (int64_t)t0 * ldk + h * kHeadDim), 0, (uint32_t)L * ldk * 2u, 0x00020000);
+        const __amdgpu_buffer_rsrc_t rv = __builtin_amdgcn_make_buffer_rsrc(
+            const_cast<uint16_t*>(v + (int64_t)t0 * ldv + h * kHeadDim), 0, (uint32_t)L * ldv * 2u, 0x00020000);
+        const int rows = (L + 31) & ~31;  // whole 32-key chunks; rows past L arrive as zeros
+        attn_barrier();                  // the previous pair is done with the LDS rows
+        // a wave copy fills one 1 KB block = 8 rows: lane -> row 8*blk + lane/8, physical chunk lane%8
+        for (int blk = wave; blk < rows / 8; blk += kAttnWaves) {
+            const int row = blk * 8 + lane / 8;
+            const int logical = (lane % 8) ^ (row & 7);
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(rk, (lds_void_t*)(kvs + blk * 512), 16, row * ldk * 2 + logical * 16, 0, 0, 0);
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(rv, (lds_void_t*)(kvs + kAttnKVElems + blk * 512), 16,
+                                                     row * ldv * 2 + logical * 16, 0, 0, 0);
         }
-        // ---- exact softmax statistics over the whole row (4 lanes share a row)
-        mrow = fmaxf(mrow, __shfl_xor(mrow, 16, kWave));
-        mrow = fmaxf(mrow, __shfl_xor(mrow, 32, kWave));
-        float lsum = 0.f;
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+        attn_barrier();
+        const uint16_t* ks_ = kvs;
+        const uint16_t* vs_ = kvs + kAttnKVElems;
+        const int nc = rows / 32;  // key chunks
+        for (int qb = wave; qb * 32 < L; qb += kAttnWaves) {
+            const int qi = min(qb * 32 + l32, L - 1);
+            const uint16_t* qrow = q + (int64_t)(t0 + qi) * ldq + h * kHeadDim + 8 * h2;
+            bf16x8 qf[4];
 #pragma unroll
-        for (int kt = 0; kt < kFusedMaxTiles; ++kt)
-            if (kt < nkt)
+            for (int ks = 0; ks < 4; ++ks) qf[ks] = as_bf16x8(ld16(qrow + 16 * ks));
+            // bf16 scores of chunk c: sv[r] for key 32c + 8*(r/4) + 4*h2 + r%4 (-inf past the sequence)
+            auto scores = [&](int c, float (&sv)[16]) {
+                floatx16 acc;
 #pragma unroll
-                for (int e = 0; e < 8; ++e)
-                    lsum += __expf(lo_bf16(sp[kt][e]) - mrow) + __expf(hi_bf16(sp[kt][e]) - mrow);
-        lsum += __shfl_xor(lsum, 16, kWave);
-        lsum += __shfl_xor(lsum, 32, kWave);
-        const float inv = 1.0f / lsum;
-
-        // ---- pass 2: O = P V with P = bf16(exp(S - max) / sum)
-        floatx4 acc[4];
+                for (int r = 0; r < 16; ++r) acc[r] = 0.f;
 #pragma unroll
-        for (int cb = 0; cb < 4; ++cb) acc[cb] = floatx4{0.f, 0.f, 0.f, 0.f};
-        rw = fetch_row16(v, ldv, t0, ld_row, L, h * kHeadDim + ld_c);
-        store_v(0);
-        __syncthreads();
+                for (int ks = 0; ks < 4; ++ks) {
+                    const bf16x8 kf = as_bf16x8(*reinterpret_cast<const u32x4*>(ks_ + kv_off(32 * c + l32, 16 * ks + 8 * h2)));
+                    acc = mfma32x32x16(kf, qf[ks], acc);
+                }
+                if (32 * (c + 1) <= L) {  // whole chunk inside the sequence (wave-uniform)
 #pragma unroll
-        for (int kt = 0; kt < kFusedMaxTiles; ++kt) {
-            if (kt < nkt) {
-                const int cur = kt & 1;
-                if (kt + 1 < nkt) rw = fetch_row16(v, ldv, t0, (kt + 1) * kTile + ld_row, L, h * kHeadDim + ld_c);
+                    for (int r = 0; r < 16; ++r) sv[r] = bf16_round(acc[r] * scale);
+                } else {
 #pragma unroll
-                for (int ks = 0; ks < 2; ++ks) {
+                    for (int r = 0; r < 16; ++r) {
+                        const int key = 32 * c + 8 * (r / 4) + 4 * h2 + (r % 4);
+                        sv[r] = key < L ? bf16_round(acc[r] * scale) : -INFINITY;
+                    }
+                }
+            };
+            // exp(s - m) is evaluated as exp2(s * log2(e) - m * log2(e)): one FMA and v_exp_f32
+            // (which flushes results below 2^-126 to zero, immaterial next to the row sum)
+            constexpr float kLog2e = 1.4426950408889634f;
+            float m_run = -INFINITY, l_run = 0.f;
+            for (int c = 0; c < nc; ++c) {
+                float sv[16];
+                scores(c, sv);
+                float cmax = -INFINITY;
+#pragma unroll
+                for (int r = 0; r < 16; ++r) cmax = fmaxf(cmax, sv[r]);
+                cmax = fmaxf(cmax, __shfl_xor(cmax, 32, kWave));  // the row's other 16 keys
+                const float m_new = fmaxf(m_run, cmax);
+                const float ml = m_new * kLog2e;
+                float csum = 0.f;
+#pragma unroll
+                for (int r = 0; r < 16; ++r) csum += __builtin_amdgcn_exp2f(fmaf(sv[r], kLog2e, -ml));
+                l_run = l_run * __builtin_amdgcn_exp2f((m_run - m_new) * kLog2e) + csum;
+                m_run = m_new;
+            }
+            const float inv = 1.0f / (l_run + __shfl_xor(l_run, 32, kWave));
+            const float ml = m_run * kLog2e;
+            floatx16 oacc[2];
+#pragma unroll
+            for (int cb = 0; cb < 2; ++cb)
+#pragma unroll
+                for (int r = 0; r < 16; ++r) oacc[cb][r] = 0.f;
+            for (int c = 0; c < nc; ++c) {
+                float sv[16];
+                scores(c, sv);
+#pragma unroll
+                for (int t = 0; t < 2; ++t) {  // 16-key steps
                     u32x4 pw;
 #pragma unroll
-                    for (int e = 0; e < 4; ++e) {
-                        const uint32_t sw = sp[kt][ks * 4 + e];
-                        pw[e] = pack_bf16x2(__expf(lo_bf16(sw) - mrow) * inv, __expf(hi_bf16(sw) - mrow) * inv);
-                    }
+                    for (int e = 0; e < 4; ++e)
+                        pw[e] = pack_bf16x2(__builtin_amdgcn_exp2f(fmaf(sv[8 * t + 2 * e], kLog2e, -ml)) * inv,
+                                            __builtin_amdgcn_exp2f(fmaf(sv[8 * t + 2 * e + 1], kLog2e, -ml)) * inv);
                     const bf16x8 pb = as_bf16x8(pw);
 #pragma unroll
-                    for (int cb = 0; cb < 4; ++cb) {
-                        const uint16_t* vrow = &Vt[cur][cb * 16 + l16][32 * ks + 4 * q4];
-                        const u32x2 lo = *reinterpret_cast<const u32x2*>(vrow);
-                        const u32x2 hi = *reinterpret_cast<const u32x2*>(vrow + 16);
-                        acc[cb] = mfma16x16x32(as_bf16x8(u32x4{lo[0], lo[1], hi[0], hi[1]}), pb, acc[cb]);
+                    for (int cb = 0; cb < 2; ++cb) {
+                        const int col = 32 * cb + 16 * (tr_g & 1) + 4 * tr_q;
+                        const int r0 = 32 * c + 16 * t + 4 * (tr_g >> 1) + tr_e;
+                        const short4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_short4_t*)(vs_ + kv_off(r0, col)));
+                        const short4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_short4_t*)(vs_ + kv_off(r0 + 8, col)));
+                        const u32x4 va = {(uint32_t)(uint16_t)lo[0] | ((uint32_t)(uint16_t)lo[1] << 16),
+                                          (uint32_t)(uint16_t)lo[2] | ((uint32_t)(uint16_t)lo[3] << 16),
+                                          (uint32_t)(uint16_t)hi[0] | ((uint32_t)(uint16_t)hi[1] << 16),
+                                          (uint32_t)(uint16_t)hi[2] | ((uint32_t)(uint16_t)hi[3] << 16)};
+                        oacc[cb] = mfma32x32x16(as_bf16x8(va), pb, oacc[cb]);
                     }
                 }
-                if (kt + 1 < nkt) store_v(cur ^ 1);
-                __syncthreads();
             }
-        }
-        const int i = ti * kTile + wave * 16 + l16;
-        if (i < L) {
-            uint16_t* orow = O + (int64_t)(t0 + i) * ldo + h * kHeadDim;
+            // O^T accumulator: lane holds channels 32*cb + 8*(r/4) + 4*h2 + r%4 of query l32
+            const int i = qb * 32 + l32;
+            if (i < L) {
+                uint16_t* orow = O + (int64_t)(t0 + i) * ldo + h * kHeadDim;
 #pragma unroll
-            for (int cb = 0; cb < 4; ++cb) {
-                const u32x2 w2 = {pack_bf16x2(acc[cb][0], acc[cb][1]), pack_bf16x2(acc[cb][2], acc[cb][3])};
-                *reinterpret_cast<u32x2*>(orow + cb * 16 + 4 * q4) = w2;
+                for (int cb = 0; cb < 2; ++cb)
+#pragma unroll
+                    for (int g = 0; g < 4; ++g) {
+                        const u32x2 w2 = {pack_bf16x2(oacc[cb][4 * g], oacc[cb][4 * g + 1]),
+                                          pack_bf16x2(oacc[cb][4 * g + 2], oacc[cb][4 * g + 3])};
+                        *reinterpret_cast<u32x2*>(orow + 32 * cb + 8 * g + 4 * h2) = w2;
+                    }
             }
         }
     }
@@ -574,12 +582,20 @@ hipError_t launch_attn_v(const PlanView& p, int dtype, const void* probs, int64_
 
 hipError_t launch_fused_attention(const PlanView& p, int dtype, const void* q, int ldq, const void* k, int ldk,
                                   const void* v, int ldv, float scale, void* out, int ldo, hipStream_t s) {
-    if (dtype != 1) return hipErrorInvalidValue;
+    if (dtype != 1 || p.max_len > kAttnMaxLen) return hipErrorInvalidValue;
+    static bool attr_set = false;  // benign race: every thread sets the same value
+    if (!attr_set) {
+        hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_attention_bf16),
+                                           hipFuncAttributeMaxDynamicSharedMemorySize, (int)kAttnLds);
+        if (e != hipSuccess) return e;
+        attr_set = true;
+    }
     const PlanArgs pa = plan_args(p);
-    const int grid = persistent_grid(p.av_cap, 4);
-    hipLaunchKernelGGL(k_attention_bf16, dim3(grid), dim3(256), 0, s, pa, static_cast<const uint16_t*>(q), ldq,
-                       static_cast<const uint16_t*>(k), ldk, static_cast<const uint16_t*>(v), ldv, scale,
-                       static_cast<uint16_t*>(out), ldo);
+    const int64_t pairs = (int64_t)p.batch * p.heads;
+    const int grid = static_cast<int>(std::min<int64_t>(pairs, device_cu_count()));
+    hipLaunchKernelGGL(k_attention_bf16, dim3(grid), dim3(kAttnThreads), kAttnLds, s, pa, p.order,
+                       static_cast<const uint16_t*>(q), ldq, static_cast<const uint16_t*>(k), ldk,
+                       static_cast<const uint16_t*>(v), ldv, scale, static_cast<uint16_t*>(out), ldo);
     return hipGetLastError();
 }
 
