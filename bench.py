@@ -74,8 +74,15 @@ def padded_fraction(L, d, dff):
     return 1.0 - useful_flops(L, d, dff) / useful_flops(Lp, d, dff)
 
 
+COMMON_DEVICE_SOURCE = "paper_2110_10221_amd/csrc/device_common.h"
+
+
 def source_hash(path):
-    return hashlib.sha256(open(os.path.join(ROOT, path), "rb").read()).hexdigest()[:16]
+    """Hash of a kernel's source together with the device header it includes."""
+    h = hashlib.sha256()
+    for p in (path, COMMON_DEVICE_SOURCE):
+        h.update(open(os.path.join(ROOT, p), "rb").read())
+    return h.hexdigest()[:16]
 
 
 def load_traffic(kernel):
