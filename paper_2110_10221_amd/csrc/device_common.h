@@ -75,17 +75,21 @@ __device__ __forceinline__ float activate(float x) {
     else return x;
 }
 
-// GELU (erf form) for bf16 outputs with a branch-free erf: Abramowitz & Stegun,
+// GELU (erf form) for bf16 outputs with a branch-free erfc: Abramowitz & Stegun,
 // Handbook of Mathematical Functions, formula 7.1.26, erfc(z) ~ t*(a1 + t*(a2 +
-// t*(a3 + t*(a4 + t*a5)))) * exp(-z^2), t = 1/(1 + p z), |error in erf| <= 1.5e-7
-// (far below bf16 resolution).  1 + erf(x/sqrt2) is formed as 2 - erfc(z) or
-// erfc(z) by the sign of x, so negative inputs keep their relative accuracy.
+// t*(a3 + t*(a4 + t*a5)))) * exp(-z^2), t = 1/(1 + p z), z >= 0, |error| <= 1.5e-7
+// (far below bf16 resolution).  Since x*erf(x/sqrt2) is even in x,
+// x*Phi(x) = max(x, 0) - |x| * erfc(|x|/sqrt2) / 2, which needs no sign branch and
+// keeps the relative accuracy of the small negative branch; the 1/2 is folded into
+// the coefficients and exp(-x^2/2) is evaluated as a power of two.
 __device__ __forceinline__ float gelu_erf_fast(float x) {
-    const float z = fabsf(x) * 0.70710678118654752f;
-    const float t = 1.0f / (1.0f + 0.3275911f * z);
-    const float poly = t * (0.254829592f + t * (-0.284496736f + t * (1.421413741f + t * (-1.453152027f + t * 1.061405429f))));
-    const float q = poly * __expf(-z * z);
-    return 0.5f * x * (x >= 0.f ? 2.0f - q : q);
+    const float ax = fabsf(x);
+    const float t = __builtin_amdgcn_rcpf(fmaf(ax, 0.3275911f * 0.70710678118654752f, 1.0f));
+    const float e = __builtin_amdgcn_exp2f(x * x * (-0.5f * 1.4426950408889634f));
+    const float half_poly =
+        t * (0.5f * 0.254829592f +
+             t * (0.5f * -0.284496736f + t * (0.5f * 1.421413741f + t * (0.5f * -1.453152027f + t * (0.5f * 1.061405429f)))));
+    return fmaf(-ax, half_poly * e, fmaxf(x, 0.f));
 }
 
 template <int ACT>

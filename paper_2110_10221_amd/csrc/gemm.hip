@@ -3,11 +3,11 @@
 // fused loop over the batch and length loops, so they are plain GEMMs with
 // M = T and no padding).
 //
-// bf16: an RAG_GEMM_BM x 256 output tile per workgroup of (BM/128) x 4 waves,
-// each wave a 128 (tokens) x 64 (features) sub-tile of v_mfma_f32_32x32x16_bf16
-// accumulators (the full-rate bf16 MFMA on gfx950).  With BM = 128 a workgroup
-// needs 72 KB of LDS, so two run on each CU and one's prologue / epilogue
-// overlaps the other's K loop.
+// bf16: a BM x 256 output tile per workgroup of (BM/128) x 4 waves, each wave a
+// 128 (tokens) x 64 (features) sub-tile of v_mfma_f32_32x32x16_bf16 accumulators
+// (the full-rate bf16 MFMA on gfx950).  BM = 128 needs 72 KB of LDS, so two
+// workgroups share a CU and one's prologue / epilogue overlaps the other's K
+// loop; BM = 256 (8 waves, 128 KB) moves a third fewer operand bytes per FLOP.
 //  - Both operands are K-contiguous in memory (x is [T, K], w is [N, K]), the
 //    operand layout the MFMA wants, so tiles go to LDS untransposed.
 //  - Global -> LDS copies are bounds-checked buffer loads that write LDS
@@ -16,8 +16,8 @@
 //    T (or N) lie outside the buffer range and arrive as zeros, so the ragged
 //    last token tile needs no clamping.
 //  - The 16-byte chunk index inside an LDS row is XOR-swizzled with the row, so
-//    the fragment reads of consecutive rows spread over the banks; the copies
-//    pick their source chunk so that the swizzled slot is filled.
+//    the fragment reads of 16 consecutive rows hit 16 distinct bank groups; the
+//    copies pick their source chunk so that the swizzled slot is filled.
 //  - Software pipeline over K steps of 32: kStages LDS stages, copies issued
 //    kStages steps ahead; the x fragments of step k+1 are read into a second
 //    register set right after the barrier and its w fragments are streamed in
@@ -37,32 +37,37 @@ namespace {
 
 typedef __attribute__((address_space(3))) void lds_void_t;
 
-#ifndef RAG_GEMM_BM
-#define RAG_GEMM_BM 128
-#endif
-#ifndef RAG_GEMM_STAGES
-#define RAG_GEMM_STAGES 3
-#endif
-constexpr int BM = RAG_GEMM_BM, BN = 256, BK = 32;
-constexpr int kStages = RAG_GEMM_STAGES;
-constexpr int kWavesM = BM / 128, kWavesN = 4;
-constexpr int kGemmWaves = kWavesM * kWavesN, kGemmThreads = kGemmWaves * kWave;
+constexpr int BN = 256, BK = 32;
 constexpr int WM = 128, WN = 64;            // wave tile (tokens x features)
 constexpr int FM = WM / 32, FN = WN / 32;   // 32x32 fragments per wave
 constexpr int KSTEPS = BK / 16;             // MFMA k-steps per K step
 constexpr int kChunks = BK / 8;             // 16-byte chunks per LDS row
 constexpr int kRowsPerBlock = 64 / kChunks; // rows filled by one 1 KB wave copy
-constexpr int kStageElems = (BM + BN) * BK; // one LDS stage: x tile then w tile
-constexpr int kXBlocksPerWave = BM / kRowsPerBlock / kGemmWaves;  // 1 KB blocks of x per wave
-constexpr int kWBlocksPerWave = BN / kRowsPerBlock / kGemmWaves;  // 1 KB blocks of w per wave
-constexpr int kCopiesPerStep = kXBlocksPerWave + kWBlocksPerWave;  // copy instructions per wave per K step
-constexpr int kEpiRows = 32;                                       // tokens per epilogue slice
-constexpr int kEpilogueBytes = kEpiRows * BN * 4;
-constexpr int kLdsBytes = kStages * kStageElems * 2 > kEpilogueBytes ? kStages * kStageElems * 2 : kEpilogueBytes;
-static_assert(kStages >= 2 && kLdsBytes <= 160 * 1024, "LDS budget");
-static_assert(kXBlocksPerWave >= 1 && kWBlocksPerWave >= 1, "copy split");
+constexpr int kEpiRows = 32;                // tokens per epilogue slice
+constexpr int kGroupM = 8;                  // token tiles per group in the tile order
 
-__device__ __forceinline__ int swz(int row) { return (row >> 1) & (kChunks - 1); }
+// Tile configurations: BM = 128 (4 waves, 3 stages, 72 KB: two workgroups per CU)
+// and BM = 256 (8 waves, 4 stages, 128 KB: one workgroup of two waves per SIMD,
+// a third fewer operand bytes per FLOP).
+template <int BM>
+struct Cfg {
+    static constexpr int kWavesM = BM / 128, kWaves = kWavesM * 4, kThreads = kWaves * kWave;
+    static constexpr int kStages = BM == 128 ? 3 : 4;
+    static constexpr int kStageElems = (BM + BN) * BK;  // one LDS stage: x tile then w tile
+    static constexpr int kXBlocks = BM / kRowsPerBlock / kWaves;  // 1 KB copies of x per wave and step
+    static constexpr int kWBlocks = BN / kRowsPerBlock / kWaves;  // 1 KB copies of w per wave and step
+    static constexpr int kCopies = kXBlocks + kWBlocks;
+    static constexpr int kStageBytes = kStages * kStageElems * 2, kEpilogueBytes = kEpiRows * BN * 4;
+    static constexpr int kLdsBytes = kStageBytes > kEpilogueBytes ? kStageBytes : kEpilogueBytes;
+    static_assert(kLdsBytes <= 160 * 1024, "LDS budget");
+    static_assert(kXBlocks >= 1 && kWBlocks >= 1, "copy split");
+};
+
+// The 16-byte chunk index inside an LDS row is XOR-swizzled with bits 2-3 of the
+// row: a ds_read_b128 serves 16 lanes per cycle, here 16 consecutive rows (four
+// 64-byte rows per 256-byte bank line), which then fall on 16 distinct 16-byte
+// bank groups.
+__device__ __forceinline__ int swz(int row) { return (row >> 2) & (kChunks - 1); }
 
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
     return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, bytes, 0x00020000);
@@ -93,53 +98,60 @@ __device__ __forceinline__ bf16x8 lds_frag(const uint16_t* tile, int row, int ch
     return as_bf16x8(*reinterpret_cast<const u32x4*>(tile + row * BK + ((chunk ^ swz(row)) * 8)));
 }
 
-// Map the linear workgroup id so that each XCD (workgroups are dealt to the 8
-// XCDs round-robin) receives a contiguous range of output tiles.
-__device__ __forceinline__ int xcd_remap(int bid, int nblocks) {
+// Output tile of a linear workgroup id.  Workgroups are dealt to the 8 XCDs
+// round-robin, so the id is first remapped to give each XCD a contiguous range;
+// that range is walked in groups of kGroupM token tiles, token tile fastest, so
+// the tiles an XCD runs at once share both x rows and w rows in its L2.
+__device__ __forceinline__ void tile_coords(int bid, int nblocks, int tiles_m, int tiles_n, int& tm, int& tn) {
     const int per = nblocks / 8, rem = nblocks % 8;
     const int xcd = bid % 8, idx = bid / 8;
-    return xcd < rem ? xcd * (per + 1) + idx : rem * (per + 1) + (xcd - rem) * per + idx;
+    const int t = xcd < rem ? xcd * (per + 1) + idx : rem * (per + 1) + (xcd - rem) * per + idx;
+    const int gsz = kGroupM * tiles_n, first = (t / gsz) * kGroupM;
+    const int gm = min(tiles_m - first, kGroupM);
+    tm = first + (t % gsz) % gm;
+    tn = (t % gsz) / gm;
 }
 
 // Wait until at most `n` copy instructions of this wave are outstanding (the
 // copies complete in issue order).
+template <int C>
 __device__ __forceinline__ void wait_copies(int n) {
-    if (n >= 3 * kCopiesPerStep) asm volatile("s_waitcnt vmcnt(%0)" ::"n"(3 * kCopiesPerStep) : "memory");
-    else if (n >= 2 * kCopiesPerStep) asm volatile("s_waitcnt vmcnt(%0)" ::"n"(2 * kCopiesPerStep) : "memory");
-    else if (n >= kCopiesPerStep) asm volatile("s_waitcnt vmcnt(%0)" ::"n"(kCopiesPerStep) : "memory");
+    if (n >= 3 * C) asm volatile("s_waitcnt vmcnt(%0)" ::"n"(3 * C) : "memory");
+    else if (n >= 2 * C) asm volatile("s_waitcnt vmcnt(%0)" ::"n"(2 * C) : "memory");
+    else if (n >= C) asm volatile("s_waitcnt vmcnt(%0)" ::"n"(C) : "memory");
     else asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
 }
 
-template <int ACT, bool HAS_BIAS, bool HAS_RES>
-__global__ __launch_bounds__(kGemmThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
+template <int BM, int ACT, bool HAS_BIAS, bool HAS_RES>
+__global__ __launch_bounds__(Cfg<BM>::kThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void k_gemm_bf16(const uint16_t* __restrict__ x, int ldx, const uint16_t* __restrict__ w,
                  const uint16_t* __restrict__ bias, const uint16_t* residual, int ldr, uint16_t* y, int ldy,
-                 int T, int K, int N, int tiles_n) {
+                 int T, int K, int N, int tiles_m, int tiles_n) {
+    using C = Cfg<BM>;
+    constexpr int kStages = C::kStages, kStageElems = C::kStageElems, kCopies = C::kCopies;
     extern __shared__ __attribute__((aligned(16))) uint16_t smem[];
-    const int tile = xcd_remap(blockIdx.x, gridDim.x);
-    const int tm = tile / tiles_n, tn = tile % tiles_n;
+    int tm, tn;
+    tile_coords(blockIdx.x, gridDim.x, tiles_m, tiles_n, tm, tn);
     const int m0 = tm * BM, n0 = tn * BN;
     const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
-    const int wm = wave / kWavesN, wn = wave % kWavesN;
+    const int wm = wave / 4, wn = wave % 4;
     const int l32 = lane % 32, h2 = lane / 32;
 
     const __amdgpu_buffer_rsrc_t rx = make_rsrc(x + (int64_t)m0 * ldx, (uint32_t)min(T - m0, BM) * ldx * 2u);
     const __amdgpu_buffer_rsrc_t rw = make_rsrc(w + (int64_t)n0 * K, (uint32_t)min(N - n0, BN) * K * 2u);
-    int vx[kXBlocksPerWave], vw[kWBlocksPerWave];
+    int vx[C::kXBlocks], vw[C::kWBlocks];
 #pragma unroll
-    for (int i = 0; i < kXBlocksPerWave; ++i)
-        vx[i] = copy_voffset(lane, (wave * kXBlocksPerWave + i) * kRowsPerBlock, ldx * 2);
+    for (int i = 0; i < C::kXBlocks; ++i) vx[i] = copy_voffset(lane, (wave * C::kXBlocks + i) * kRowsPerBlock, ldx * 2);
 #pragma unroll
-    for (int i = 0; i < kWBlocksPerWave; ++i)
-        vw[i] = copy_voffset(lane, (wave * kWBlocksPerWave + i) * kRowsPerBlock, K * 2);
+    for (int i = 0; i < C::kWBlocks; ++i) vw[i] = copy_voffset(lane, (wave * C::kWBlocks + i) * kRowsPerBlock, K * 2);
     auto issue = [&](int step) {
         uint16_t* xs = smem + (step % kStages) * kStageElems;
         uint16_t* ws = xs + BM * BK;
         const int k0b = step * BK * 2;
 #pragma unroll
-        for (int i = 0; i < kXBlocksPerWave; ++i) copy_block(rx, xs + (wave * kXBlocksPerWave + i) * 512, vx[i], k0b);
+        for (int i = 0; i < C::kXBlocks; ++i) copy_block(rx, xs + (wave * C::kXBlocks + i) * 512, vx[i], k0b);
 #pragma unroll
-        for (int i = 0; i < kWBlocksPerWave; ++i) copy_block(rw, ws + (wave * kWBlocksPerWave + i) * 512, vw[i], k0b);
+        for (int i = 0; i < C::kWBlocks; ++i) copy_block(rw, ws + (wave * C::kWBlocks + i) * 512, vw[i], k0b);
     };
 
     floatx16 acc[FN][FM];
@@ -166,7 +178,7 @@ void k_gemm_bf16(const uint16_t* __restrict__ x, int ldx, const uint16_t* __rest
     // one K step with a successor: prefetch its fragments while the MFMAs run
     auto step_next = [&](bf16x8 (&fa)[KSTEPS][FN], bf16x8 (&fb)[KSTEPS][FM], bf16x8 (&na)[KSTEPS][FN],
                          bf16x8 (&nb)[KSTEPS][FM], int kt, int nk) {
-        wait_copies(min(kStages - 2, nk - 2 - kt) * kCopiesPerStep);
+        wait_copies<kCopies>(min(kStages - 2, nk - 2 - kt) * kCopies);
         barrier_lds();  // step kt+1's stage is visible; step kt's stage is no longer read
         if (kt + kStages < nk) issue(kt + kStages);
         read_x(nb, kt + 1);
@@ -192,7 +204,7 @@ void k_gemm_bf16(const uint16_t* __restrict__ x, int ldx, const uint16_t* __rest
 #pragma unroll
     for (int st = 0; st < kStages; ++st)
         if (st < nk) issue(st);
-    wait_copies(min(kStages - 1, nk - 1) * kCopiesPerStep);
+    wait_copies<kCopies>(min(kStages - 1, nk - 1) * kCopies);
     barrier_lds();
     read_x(fb0, 0);
 #pragma unroll
@@ -207,8 +219,8 @@ void k_gemm_bf16(const uint16_t* __restrict__ x, int ldx, const uint16_t* __rest
     step_next(fa0, fb0, fa1, fb1, nk - 2, nk);
     step_last(fa1, fb1);
 
-    // Epilogue through LDS, 32 tokens at a time: the wave holding a slice writes
-    // its fp32 accumulators there, then all waves read whole rows back (16 bytes
+    // Epilogue through LDS, 32 tokens at a time: the waves holding a slice write
+    // their fp32 accumulators there, then all waves read whole rows back (16 bytes
     // per lane, 256 features per row), apply bias, activation and residual and
     // store 512-byte rows.  acc[i][j][4g + r] holds (token j*32 + l32, feature
     // i*32 + 8g + 4*h2 + r) of the wave's sub-tile.  LDS layout: row r of 64
@@ -225,7 +237,7 @@ void k_gemm_bf16(const uint16_t* __restrict__ x, int ldx, const uint16_t* __rest
             bv[3] = hi_bf16(bb[1]);
         }
     }
-    constexpr int kRowsPerWave = kEpiRows / kGemmWaves;
+    constexpr int kRowsPerWave = kEpiRows / C::kWaves;
 #pragma unroll
     for (int slice = 0; slice < BM / kEpiRows; ++slice) {
         barrier_lds();  // the K loop (first slice) or the previous slice is done with LDS
@@ -312,23 +324,35 @@ __global__ __launch_bounds__(256) void k_gemm_f32(const float* __restrict__ x, i
     }
 }
 
-template <int ACT, bool HB, bool HR>
-hipError_t launch_bf16_variant(const void* x, int ldx, const void* w, const void* bias, const void* residual,
-                               int ldr, void* y, int ldy, int T, int K, int N, hipStream_t s) {
+template <int BM, int ACT, bool HB, bool HR>
+hipError_t launch_bf16_tiles(const void* x, int ldx, const void* w, const void* bias, const void* residual, int ldr,
+                             void* y, int ldy, int T, int K, int N, hipStream_t s) {
+    using C = Cfg<BM>;
     const int tiles_m = (T + BM - 1) / BM, tiles_n = (N + BN - 1) / BN;
-    const size_t lds = kLdsBytes;
     static bool attr_set = false;  // benign race: every thread sets the same value
     if (!attr_set) {
-        hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_gemm_bf16<ACT, HB, HR>),
-                                           hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+        hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_gemm_bf16<BM, ACT, HB, HR>),
+                                           hipFuncAttributeMaxDynamicSharedMemorySize, C::kLdsBytes);
         if (e != hipSuccess) return e;
         attr_set = true;
     }
-    hipLaunchKernelGGL((k_gemm_bf16<ACT, HB, HR>), dim3(tiles_m * tiles_n), dim3(kGemmThreads), lds, s,
+    hipLaunchKernelGGL((k_gemm_bf16<BM, ACT, HB, HR>), dim3(tiles_m * tiles_n), dim3(C::kThreads), C::kLdsBytes, s,
                        static_cast<const uint16_t*>(x), ldx, static_cast<const uint16_t*>(w),
                        static_cast<const uint16_t*>(bias), static_cast<const uint16_t*>(residual), ldr,
-                       static_cast<uint16_t*>(y), ldy, T, K, N, tiles_n);
+                       static_cast<uint16_t*>(y), ldy, T, K, N, tiles_m, tiles_n);
     return hipGetLastError();
+}
+
+// 256-token tiles read a third fewer operand bytes per FLOP but run one
+// workgroup per CU, so nothing hides their epilogue and their last round of
+// tiles is coarser: measured on the encoder shapes they pay off for wide
+// outputs (N >= 2048) with a plain epilogue.
+template <int ACT, bool HB, bool HR>
+hipError_t launch_bf16_variant(const void* x, int ldx, const void* w, const void* bias, const void* residual,
+                               int ldr, void* y, int ldy, int T, int K, int N, hipStream_t s) {
+    if (ACT == 0 && !HR && N >= 2048 && T >= 2048)
+        return launch_bf16_tiles<256, ACT, HB, HR>(x, ldx, w, bias, residual, ldr, y, ldy, T, K, N, s);
+    return launch_bf16_tiles<128, ACT, HB, HR>(x, ldx, w, bias, residual, ldr, y, ldy, T, K, N, s);
 }
 
 template <int ACT>

@@ -68,10 +68,19 @@ def test_empty_batch_is_a_no_op():
     torch.cuda.synchronize()
 
 
+@pytest.mark.parametrize("T", [2048, 2049, 3001])
+@pytest.mark.parametrize("K,N", [(128, 2112), (192, 3072)])
+def test_wide_outputs_ragged_tails(T, K, N):
+    # wide outputs with a plain epilogue take the 256-token tiles: ragged token and feature tails
+    got, ref = _linear("bf16", T, K, N, oracle.ACT_NONE, True, False, seed=T + N)
+    assert close(got, ref, "bf16")
+
+
 @pytest.mark.parametrize("K,N,act,res", [(1024, 3072, 0, False), (1024, 1024, 0, True), (1024, 4096, 1, False),
                                          (4096, 1024, 0, True)])
 def test_layer_shapes_full_token_count_sampled_rows(K, N, act, res):
-    # config-4 GEMM shapes at a config-4-sized token count; the oracle checks 96 sampled rows
+    # the four GEMMs of a d_model 1024 / FFN 4096 layer at 35475 tokens (batch 128,
+    # lengths uniform in [32, 512]); the oracle checks 96 sampled rows
     T = 35475
     rows = np.r_[0:32, T // 2:T // 2 + 32, T - 32:T]
     got, ref = _linear("bf16", T, K, N, act, True, res, seed=N, rows=rows)
