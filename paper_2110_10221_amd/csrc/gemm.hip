@@ -238,6 +238,18 @@ void k_gemm_bf16(const uint16_t* __restrict__ x, int ldx, const uint16_t* __rest
         }
     }
     constexpr int kRowsPerWave = kEpiRows / C::kWaves;
+    // Residual rows are fetched for every slice at once, so their latency is paid once per tile.
+    u32x2 res[HAS_RES ? BM / kEpiRows : 1][kRowsPerWave];
+    if constexpr (HAS_RES) {
+#pragma unroll
+        for (int slice = 0; slice < BM / kEpiRows; ++slice)
+#pragma unroll
+            for (int rr = 0; rr < kRowsPerWave; ++rr) {
+                const int m = m0 + slice * kEpiRows + wave * kRowsPerWave + rr;
+                res[slice][rr] = (m < T && ncol < N) ? *reinterpret_cast<const u32x2*>(residual + (int64_t)m * ldr + ncol)
+                                                     : u32x2{0u, 0u};
+            }
+    }
 #pragma unroll
     for (int slice = 0; slice < BM / kEpiRows; ++slice) {
         barrier_lds();  // the K loop (first slice) or the previous slice is done with LDS
@@ -263,7 +275,7 @@ void k_gemm_bf16(const uint16_t* __restrict__ x, int ldx, const uint16_t* __rest
 #pragma unroll
                 for (int e = 0; e < 4; ++e) v[e] = activate_bf16<ACT>(o[e] + bv[e]);
                 if constexpr (HAS_RES) {
-                    const u32x2 rv = *reinterpret_cast<const u32x2*>(residual + (int64_t)m * ldr + ncol);
+                    const u32x2 rv = res[HAS_RES ? slice : 0][rr];
                     v[0] += lo_bf16(rv[0]);
                     v[1] += hi_bf16(rv[0]);
                     v[2] += lo_bf16(rv[1]);
@@ -350,8 +362,10 @@ hipError_t launch_bf16_tiles(const void* x, int ldx, const void* w, const void* 
 template <int ACT, bool HB, bool HR>
 hipError_t launch_bf16_variant(const void* x, int ldx, const void* w, const void* bias, const void* residual,
                                int ldr, void* y, int ldy, int T, int K, int N, hipStream_t s) {
-    if (ACT == 0 && !HR && N >= 2048 && T >= 2048)
-        return launch_bf16_tiles<256, ACT, HB, HR>(x, ldx, w, bias, residual, ldr, y, ldy, T, K, N, s);
+    if constexpr (ACT == 0 && !HR) {
+        if (N >= 2048 && T >= 2048)
+            return launch_bf16_tiles<256, ACT, HB, HR>(x, ldx, w, bias, residual, ldr, y, ldy, T, K, N, s);
+    }
     return launch_bf16_tiles<128, ACT, HB, HR>(x, ldx, w, bias, residual, ldr, y, ldy, T, K, N, s);
 }
 
