@@ -361,27 +361,29 @@ __global__ __launch_bounds__(256) void k_attn_v_f32(PlanArgs pa, const float* __
 
 // ---------------------------------------------------------------------------
 // Fused ragged attention: QK^T, softmax and Attn.V of one (sequence b, head h)
-// pair per workgroup of eight waves, with the same rounding points as the
-// three separate operators: scores rounded to bf16, an exact softmax over the
-// whole row, probabilities rounded to bf16, fp32 accumulation of P.V.  No
-// score reaches memory.
-//   load    the pair's K and V rows (at most RAG_FUSED_MAX_LEN of them) are
-//           copied once into LDS with bounds-checked buffer loads that write
-//           LDS directly (16-byte chunks XOR-swizzled by row)
-//   then each wave takes 32-query blocks of the sequence in turn:
-//   pass 1  S^T = K Q^T per 32 keys with v_mfma_f32_32x32x16_bf16 (lane holds
-//           query i = lane % 32 and keys 8*(r/4) + 4*(lane/32) + r%4), round to
-//           bf16, keep the running row maximum and the running sum of
-//           exp(s - max) (rescaled when the maximum grows)
-//   pass 2  recompute the same bf16 scores, form p = bf16(exp(s - max) / sum)
-//           and accumulate O^T = V^T P^T.  The lane's eight keys of each 16-key
-//           step {4h..4h+3, 8+4h..8+4h+3} (h = lane/32) are its k values (the
-//           MFMA pairs the k-th element of A with the k-th element of B), and
-//           ds_read_b64_tr_b16 gathers the V operand for exactly those keys
-//           from the row-major V rows.
-// Pairs are taken longest sequence first (the plan's order), so the largest
-// blocks of work start first.  Recomputing the scores costs one extra QK^T but
-// keeps the registers low enough for two waves per SIMD.
+// pair per workgroup of eight waves in a single pass over the keys; no score
+// reaches memory.
+//   load   the pair's K and V rows (at most RAG_FUSED_MAX_LEN of them) are
+//          copied once into LDS with bounds-checked buffer loads that write
+//          LDS directly (16-byte chunks XOR-swizzled by row)
+//   then each wave takes 32-query blocks of the sequence in turn and walks the
+//   keys 32 at a time:
+//   scores S^T = K Q^T with v_mfma_f32_32x32x16_bf16 (lane holds query
+//          i = lane % 32 and keys 8*(r/4) + 4*(lane/32) + r%4), kept in fp32
+//   softmax online: z = s * scale * log2(e); a per-row reference m, raised
+//          only when a chunk's maximum exceeds it by more than 8 (so
+//          exp2(z - m) <= 2^8 and the rescaling of the running sum and output
+//          is rare); e = exp2(z - m) rounded to bf16 is the MFMA operand
+//   output O^T += V^T E^T.  The lane's eight keys of each 16-key step
+//          {4h..4h+3, 8+4h..8+4h+3} (h = lane/32) are its k values (the MFMA
+//          pairs the k-th element of A with the k-th element of B), and
+//          ds_read_b64_tr_b16 gathers the V operand for exactly those keys
+//          from the row-major V rows; O is divided by the row sum at the end.
+// Relative to the three separate operators, the fused path skips the bf16
+// rounding of the scores and rounds the unnormalised exponentials instead of
+// the probabilities (the flash-attention order); both differ from the
+// separate path by rounding only.  Pairs are taken longest sequence first (the
+// plan's order), so the largest blocks of work start first.
 // ---------------------------------------------------------------------------
 
 typedef __attribute__((address_space(3))) void lds_void_t;
@@ -392,14 +394,24 @@ constexpr int kAttnWaves = 8, kAttnThreads = kAttnWaves * kWave;
 constexpr int kAttnMaxLen = 512;                         // RAG_FUSED_MAX_LEN
 constexpr int kAttnKVElems = kAttnMaxLen * kHeadDim;      // one of K or V in LDS
 constexpr size_t kAttnLds = 2 * kAttnKVElems * sizeof(uint16_t);
-
-__device__ __forceinline__ float bf16_round(float x) { return bf16_to_f32(f32_to_bf16(x)); }
+constexpr float kRescaleSlack = 8.f;                      // log2 of the largest exponential kept
 
 // Element offset of (row, col) in [rows][64 channels] LDS storage whose 16-byte
 // chunks are XOR-swizzled by the row.
 __device__ __forceinline__ int kv_off(int row, int col) { return row * kHeadDim + ((((col >> 3) ^ row) & 7) << 3) + (col & 7); }
 
 __device__ __forceinline__ void attn_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+
+// Combine a value with the one held by the lane 32 apart (the other half of
+// the same query row): v_permlane32_swap hands each half the other's value.
+__device__ __forceinline__ float max_xor32(float v) {
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float sum_xor32(float v) {
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
 
 __global__ __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void k_attention_bf16(PlanArgs pa, const int32_t* __restrict__ order, const uint16_t* __restrict__ q, int ldq,
@@ -413,6 +425,9 @@ void k_attention_bf16(PlanArgs pa, const int32_t* __restrict__ order, const uint
     const int l32 = lane % 32, h2 = lane / 32;
     // transposed-read addressing inside a 16-lane group (see the header comment)
     const int tr_e = (lane % 16) / 4, tr_q = lane % 4, tr_g = lane / 16;
+    // z = s * scale * log2(e) with a non-negative factor: a negative scale flips the sign of q instead
+    const float zs = fabsf(scale) * 1.4426950408889634f;
+    const uint32_t qsign = scale < 0.f ? 0x80008000u : 0u;
 
     for (int pair = blockIdx.x; pair < n_pairs; pair += gridDim.x) {
         const int b = order[pair / H], h = pair % H;
@@ -438,76 +453,74 @@ void k_attention_bf16(PlanArgs pa, const int32_t* __restrict__ order, const uint
         const uint16_t* ks_ = kvs;
         const uint16_t* vs_ = kvs + kAttnKVElems;
         const int nc = rows / 32;  // key chunks
+        // 32*c and 16*t leave the low three row bits (the swizzle's) unchanged, so
+        // the LDS offsets of chunk c are those of chunk 0 plus 32*c rows.
+        int koff[4], voff[2];
+#pragma unroll
+        for (int ks = 0; ks < 4; ++ks) koff[ks] = kv_off(l32, 16 * ks + 8 * h2);
+#pragma unroll
+        for (int cb = 0; cb < 2; ++cb) voff[cb] = kv_off(4 * (tr_g >> 1) + tr_e, 32 * cb + 16 * (tr_g & 1) + 4 * tr_q);
         for (int qb = wave; qb * 32 < L; qb += kAttnWaves) {
             const int qi = min(qb * 32 + l32, L - 1);
             const uint16_t* qrow = q + (int64_t)(t0 + qi) * ldq + h * kHeadDim + 8 * h2;
             bf16x8 qf[4];
 #pragma unroll
-            for (int ks = 0; ks < 4; ++ks) qf[ks] = as_bf16x8(ld16(qrow + 16 * ks));
-            // bf16 scores of chunk c: sv[r] for key 32c + 8*(r/4) + 4*h2 + r%4 (-inf past the sequence)
-            auto scores = [&](int c, float (&sv)[16]) {
-                floatx16 acc;
-#pragma unroll
-                for (int r = 0; r < 16; ++r) acc[r] = 0.f;
-#pragma unroll
-                for (int ks = 0; ks < 4; ++ks) {
-                    const bf16x8 kf = as_bf16x8(*reinterpret_cast<const u32x4*>(ks_ + kv_off(32 * c + l32, 16 * ks + 8 * h2)));
-                    acc = mfma32x32x16(kf, qf[ks], acc);
-                }
-                if (32 * (c + 1) <= L) {  // whole chunk inside the sequence (wave-uniform)
-#pragma unroll
-                    for (int r = 0; r < 16; ++r) sv[r] = bf16_round(acc[r] * scale);
-                } else {
-#pragma unroll
-                    for (int r = 0; r < 16; ++r) {
-                        const int key = 32 * c + 8 * (r / 4) + 4 * h2 + (r % 4);
-                        sv[r] = key < L ? bf16_round(acc[r] * scale) : -INFINITY;
-                    }
-                }
-            };
-            // exp(s - m) is evaluated as exp2(s * log2(e) - m * log2(e)): one FMA and v_exp_f32
-            // (which flushes results below 2^-126 to zero, immaterial next to the row sum)
-            constexpr float kLog2e = 1.4426950408889634f;
-            float m_run = -INFINITY, l_run = 0.f;
-            for (int c = 0; c < nc; ++c) {
-                float sv[16];
-                scores(c, sv);
-                float cmax = -INFINITY;
-#pragma unroll
-                for (int r = 0; r < 16; ++r) cmax = fmaxf(cmax, sv[r]);
-                cmax = fmaxf(cmax, __shfl_xor(cmax, 32, kWave));  // the row's other 16 keys
-                const float m_new = fmaxf(m_run, cmax);
-                const float ml = m_new * kLog2e;
-                float csum = 0.f;
-#pragma unroll
-                for (int r = 0; r < 16; ++r) csum += __builtin_amdgcn_exp2f(fmaf(sv[r], kLog2e, -ml));
-                l_run = l_run * __builtin_amdgcn_exp2f((m_run - m_new) * kLog2e) + csum;
-                m_run = m_new;
+            for (int ks = 0; ks < 4; ++ks) {
+                u32x4 raw = ld16(qrow + 16 * ks);
+                raw ^= qsign;
+                qf[ks] = as_bf16x8(raw);
             }
-            const float inv = 1.0f / (l_run + __shfl_xor(l_run, 32, kWave));
-            const float ml = m_run * kLog2e;
+            float m = -INFINITY, lsum = 0.f;
             floatx16 oacc[2];
 #pragma unroll
             for (int cb = 0; cb < 2; ++cb)
 #pragma unroll
                 for (int r = 0; r < 16; ++r) oacc[cb][r] = 0.f;
             for (int c = 0; c < nc; ++c) {
-                float sv[16];
-                scores(c, sv);
+                floatx16 acc;
+#pragma unroll
+                for (int r = 0; r < 16; ++r) acc[r] = 0.f;
+#pragma unroll
+                for (int ks = 0; ks < 4; ++ks) {
+                    const bf16x8 kf = as_bf16x8(*reinterpret_cast<const u32x4*>(ks_ + 32 * kHeadDim * c + koff[ks]));
+                    acc = mfma32x32x16(kf, qf[ks], acc);
+                }
+                if (32 * (c + 1) > L) {  // keys past the sequence take no part (wave-uniform branch)
+#pragma unroll
+                    for (int r = 0; r < 16; ++r)
+                        if (32 * c + 8 * (r / 4) + 4 * h2 + (r % 4) >= L) acc[r] = -INFINITY;
+                }
+                float cmax = acc[0];
+#pragma unroll
+                for (int r = 1; r < 16; ++r) cmax = fmaxf(cmax, acc[r]);
+                const float cz = max_xor32(cmax) * zs;
+                const bool raise = cz > m + kRescaleSlack;
+                if (__ballot(raise) != 0) {  // rare after the first chunk
+                    const float mn = raise ? cz : m;
+                    const float alpha = raise ? __builtin_amdgcn_exp2f(m - mn) : 1.f;  // 0 on the first chunk
+                    lsum *= alpha;
+#pragma unroll
+                    for (int cb = 0; cb < 2; ++cb)
+#pragma unroll
+                        for (int r = 0; r < 16; ++r) oacc[cb][r] *= alpha;
+                    m = mn;
+                }
 #pragma unroll
                 for (int t = 0; t < 2; ++t) {  // 16-key steps
                     u32x4 pw;
 #pragma unroll
-                    for (int e = 0; e < 4; ++e)
-                        pw[e] = pack_bf16x2(__builtin_amdgcn_exp2f(fmaf(sv[8 * t + 2 * e], kLog2e, -ml)) * inv,
-                                            __builtin_amdgcn_exp2f(fmaf(sv[8 * t + 2 * e + 1], kLog2e, -ml)) * inv);
+                    for (int e = 0; e < 4; ++e) {
+                        const float e0 = __builtin_amdgcn_exp2f(fmaf(acc[8 * t + 2 * e], zs, -m));
+                        const float e1 = __builtin_amdgcn_exp2f(fmaf(acc[8 * t + 2 * e + 1], zs, -m));
+                        lsum += e0 + e1;
+                        pw[e] = pack_bf16x2(e0, e1);
+                    }
                     const bf16x8 pb = as_bf16x8(pw);
 #pragma unroll
                     for (int cb = 0; cb < 2; ++cb) {
-                        const int col = 32 * cb + 16 * (tr_g & 1) + 4 * tr_q;
-                        const int r0 = 32 * c + 16 * t + 4 * (tr_g >> 1) + tr_e;
-                        const short4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_short4_t*)(vs_ + kv_off(r0, col)));
-                        const short4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_short4_t*)(vs_ + kv_off(r0 + 8, col)));
+                        const uint16_t* vp = vs_ + (32 * c + 16 * t) * kHeadDim + voff[cb];
+                        const short4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_short4_t*)vp);
+                        const short4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_short4_t*)(vp + 8 * kHeadDim));
                         const u32x4 va = {(uint32_t)(uint16_t)lo[0] | ((uint32_t)(uint16_t)lo[1] << 16),
                                           (uint32_t)(uint16_t)lo[2] | ((uint32_t)(uint16_t)lo[3] << 16),
                                           (uint32_t)(uint16_t)hi[0] | ((uint32_t)(uint16_t)hi[1] << 16),
@@ -516,6 +529,7 @@ void k_attention_bf16(PlanArgs pa, const int32_t* __restrict__ order, const uint
                     }
                 }
             }
+            const float inv = 1.0f / sum_xor32(lsum);
             // O^T accumulator: lane holds channels 32*cb + 8*(r/4) + 4*h2 + r%4 of query l32
             const int i = qb * 32 + l32;
             if (i < L) {
@@ -524,8 +538,8 @@ void k_attention_bf16(PlanArgs pa, const int32_t* __restrict__ order, const uint
                 for (int cb = 0; cb < 2; ++cb)
 #pragma unroll
                     for (int g = 0; g < 4; ++g) {
-                        const u32x2 w2 = {pack_bf16x2(oacc[cb][4 * g], oacc[cb][4 * g + 1]),
-                                          pack_bf16x2(oacc[cb][4 * g + 2], oacc[cb][4 * g + 3])};
+                        const u32x2 w2 = {pack_bf16x2(oacc[cb][4 * g] * inv, oacc[cb][4 * g + 1] * inv),
+                                          pack_bf16x2(oacc[cb][4 * g + 2] * inv, oacc[cb][4 * g + 3] * inv)};
                         *reinterpret_cast<u32x2*>(orow + 32 * cb + 8 * g + 4 * h2) = w2;
                     }
             }
