@@ -361,8 +361,8 @@ __global__ __launch_bounds__(256) void k_attn_v_f32(PlanArgs pa, const float* __
 
 // ---------------------------------------------------------------------------
 // Fused ragged attention: QK^T, softmax and Attn.V of one (sequence b, head h)
-// pair per workgroup of eight waves in a single pass over the keys; no score
-// reaches memory.
+// pair per workgroup of sixteen waves (four per SIMD) in a single pass over
+// the keys; no score reaches memory.
 //   load   the pair's K and V rows (at most RAG_FUSED_MAX_LEN of them) are
 //          copied once into LDS with bounds-checked buffer loads that write
 //          LDS directly (16-byte chunks XOR-swizzled by row)
@@ -390,15 +390,22 @@ typedef __attribute__((address_space(3))) void lds_void_t;
 typedef __attribute__((ext_vector_type(4))) short short4_t;
 typedef __attribute__((address_space(3))) short4_t lds_short4_t;
 
-constexpr int kAttnWaves = 8, kAttnThreads = kAttnWaves * kWave;
+#ifndef RAG_ATTN_WAVES
+#define RAG_ATTN_WAVES 16
+#endif
+constexpr int kAttnWaves = RAG_ATTN_WAVES, kAttnThreads = kAttnWaves * kWave;
 constexpr int kAttnMaxLen = 512;                         // RAG_FUSED_MAX_LEN
 constexpr int kAttnKVElems = kAttnMaxLen * kHeadDim;      // one of K or V in LDS
 constexpr size_t kAttnLds = 2 * kAttnKVElems * sizeof(uint16_t);
 constexpr float kRescaleSlack = 8.f;                      // log2 of the largest exponential kept
 
-// Element offset of (row, col) in [rows][64 channels] LDS storage whose 16-byte
-// chunks are XOR-swizzled by the row.
-__device__ __forceinline__ int kv_off(int row, int col) { return row * kHeadDim + ((((col >> 3) ^ row) & 7) << 3) + (col & 7); }
+// Element offset of (row, col) in [rows][64 channels] LDS storage (128-byte rows,
+// two per 256-byte bank line) whose 16-byte chunks are XOR-swizzled by row bits
+// 1-3: the K-operand reads (16 consecutive rows, one chunk each) then meet 16
+// distinct bank groups, and in the transposed V reads (rows r..r+3, four
+// adjacent chunks each) rows r and r+2 use opposite halves of the row.
+__device__ __forceinline__ int kv_swz(int row) { return (((row >> 1) & 1) << 2) | ((row >> 2) & 3); }
+__device__ __forceinline__ int kv_off(int row, int col) { return row * kHeadDim + ((((col >> 3) ^ kv_swz(row)) & 7) << 3) + (col & 7); }
 
 __device__ __forceinline__ void attn_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
 
@@ -408,12 +415,13 @@ __device__ __forceinline__ float max_xor32(float v) {
     const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
     return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
 }
+
 __device__ __forceinline__ float sum_xor32(float v) {
     const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
     return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
-__global__ __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
+__global__ __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(kAttnWaves / 4, kAttnWaves / 4)))
 void k_attention_bf16(PlanArgs pa, const int32_t* __restrict__ order, const uint16_t* __restrict__ q, int ldq,
                       const uint16_t* __restrict__ k, int ldk, const uint16_t* __restrict__ v, int ldv, float scale,
                       uint16_t* __restrict__ O, int ldo) {
@@ -443,7 +451,7 @@ void k_attention_bf16(PlanArgs pa, const int32_t* __restrict__ order, const uint
         // a wave copy fills one 1 KB block = 8 rows: lane -> row 8*blk + lane/8, physical chunk lane%8
         for (int blk = wave; blk < rows / 8; blk += kAttnWaves) {
             const int row = blk * 8 + lane / 8;
-            const int logical = (lane % 8) ^ (row & 7);
+            const int logical = (lane % 8) ^ kv_swz(row);
             __builtin_amdgcn_raw_ptr_buffer_load_lds(rk, (lds_void_t*)(kvs + blk * 512), 16, row * ldk * 2 + logical * 16, 0, 0, 0);
             __builtin_amdgcn_raw_ptr_buffer_load_lds(rv, (lds_void_t*)(kvs + kAttnKVElems + blk * 512), 16,
                                                      row * ldv * 2 + logical * 16, 0, 0, 0);
@@ -453,13 +461,16 @@ void k_attention_bf16(PlanArgs pa, const int32_t* __restrict__ order, const uint
         const uint16_t* ks_ = kvs;
         const uint16_t* vs_ = kvs + kAttnKVElems;
         const int nc = rows / 32;  // key chunks
-        // 32*c and 16*t leave the low three row bits (the swizzle's) unchanged, so
-        // the LDS offsets of chunk c are those of chunk 0 plus 32*c rows.
-        int koff[4], voff[2];
+        // 32*c and 16*t leave row bits 1-3 (the swizzle's) unchanged, so the LDS
+        // offsets of chunk c are those of chunk 0 plus 32*c rows.
+        int koff[4], voff[2][2];
 #pragma unroll
         for (int ks = 0; ks < 4; ++ks) koff[ks] = kv_off(l32, 16 * ks + 8 * h2);
 #pragma unroll
-        for (int cb = 0; cb < 2; ++cb) voff[cb] = kv_off(4 * (tr_g >> 1) + tr_e, 32 * cb + 16 * (tr_g & 1) + 4 * tr_q);
+        for (int cb = 0; cb < 2; ++cb)
+#pragma unroll
+            for (int hi = 0; hi < 2; ++hi)
+                voff[cb][hi] = kv_off(4 * (tr_g >> 1) + tr_e + 8 * hi, 32 * cb + 16 * (tr_g & 1) + 4 * tr_q);
         for (int qb = wave; qb * 32 < L; qb += kAttnWaves) {
             const int qi = min(qb * 32 + l32, L - 1);
             const uint16_t* qrow = q + (int64_t)(t0 + qi) * ldq + h * kHeadDim + 8 * h2;
@@ -471,7 +482,7 @@ void k_attention_bf16(PlanArgs pa, const int32_t* __restrict__ order, const uint
                 qf[ks] = as_bf16x8(raw);
             }
             float m = -INFINITY, lsum = 0.f;
-            floatx16 oacc[2];
+            floatx16 oacc[2];  // O^T, channels 0-31 and 32-63
 #pragma unroll
             for (int cb = 0; cb < 2; ++cb)
 #pragma unroll
@@ -518,9 +529,9 @@ void k_attention_bf16(PlanArgs pa, const int32_t* __restrict__ order, const uint
                     const bf16x8 pb = as_bf16x8(pw);
 #pragma unroll
                     for (int cb = 0; cb < 2; ++cb) {
-                        const uint16_t* vp = vs_ + (32 * c + 16 * t) * kHeadDim + voff[cb];
-                        const short4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_short4_t*)vp);
-                        const short4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_short4_t*)(vp + 8 * kHeadDim));
+                        const uint16_t* vp = vs_ + (32 * c + 16 * t) * kHeadDim;
+                        const short4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_short4_t*)(vp + voff[cb][0]));
+                        const short4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_short4_t*)(vp + voff[cb][1]));
                         const u32x4 va = {(uint32_t)(uint16_t)lo[0] | ((uint32_t)(uint16_t)lo[1] << 16),
                                           (uint32_t)(uint16_t)lo[2] | ((uint32_t)(uint16_t)lo[3] << 16),
                                           (uint32_t)(uint16_t)hi[0] | ((uint32_t)(uint16_t)hi[1] << 16),
