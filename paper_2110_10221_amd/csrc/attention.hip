@@ -487,15 +487,20 @@ void k_attention_bf16(PlanArgs pa, const int32_t* __restrict__ order, const uint
             for (int cb = 0; cb < 2; ++cb)
 #pragma unroll
                 for (int r = 0; r < 16; ++r) oacc[cb][r] = 0.f;
-            for (int c = 0; c < nc; ++c) {
+            // per-lane LDS pointers of chunk 0, advanced by 32 rows per chunk
+            const uint16_t* kp = ks_ + koff[0];
+            const uint16_t* vp = vs_;
+            for (int c = 0; c < nc; ++c, kp += 32 * kHeadDim, vp += 32 * kHeadDim) {
                 floatx16 acc;
 #pragma unroll
                 for (int r = 0; r < 16; ++r) acc[r] = 0.f;
+                bf16x8 kf[4];
 #pragma unroll
-                for (int ks = 0; ks < 4; ++ks) {
-                    const bf16x8 kf = as_bf16x8(*reinterpret_cast<const u32x4*>(ks_ + 32 * kHeadDim * c + koff[ks]));
-                    acc = mfma32x32x16(kf, qf[ks], acc);
-                }
+                for (int ks = 0; ks < 4; ++ks)
+                    kf[ks] = as_bf16x8(*reinterpret_cast<const u32x4*>(kp + (koff[ks] - koff[0])));
+                __builtin_amdgcn_sched_barrier(0);  // all four reads in flight before the first MFMA waits
+#pragma unroll
+                for (int ks = 0; ks < 4; ++ks) acc = mfma32x32x16(kf[ks], qf[ks], acc);
                 if (32 * (c + 1) > L) {  // keys past the sequence take no part (wave-uniform branch)
 #pragma unroll
                     for (int r = 0; r < 16; ++r)
@@ -529,9 +534,9 @@ void k_attention_bf16(PlanArgs pa, const int32_t* __restrict__ order, const uint
                     const bf16x8 pb = as_bf16x8(pw);
 #pragma unroll
                     for (int cb = 0; cb < 2; ++cb) {
-                        const uint16_t* vp = vs_ + (32 * c + 16 * t) * kHeadDim;
-                        const short4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_short4_t*)(vp + voff[cb][0]));
-                        const short4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_short4_t*)(vp + voff[cb][1]));
+                        const uint16_t* vt = vp + 16 * t * kHeadDim;
+                        const short4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_short4_t*)(vt + voff[cb][0]));
+                        const short4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_short4_t*)(vt + voff[cb][1]));
                         const u32x4 va = {(uint32_t)(uint16_t)lo[0] | ((uint32_t)(uint16_t)lo[1] << 16),
                                           (uint32_t)(uint16_t)lo[2] | ((uint32_t)(uint16_t)lo[3] << 16),
                                           (uint32_t)(uint16_t)hi[0] | ((uint32_t)(uint16_t)hi[1] << 16),
