@@ -9,6 +9,7 @@
 //   2. rank   (B/256 workgroups): stable longest-first rank -> order
 //   3. items  (one workgroup): per-sequence item counts scanned in `order`
 //   4. fill   (B workgroups): work-list entries and the token map
+// Batches of up to 1024 sequences run steps 1-3 as one single-workgroup kernel.
 #include <climits>
 
 #include "device_common.h"
@@ -166,6 +167,83 @@ __global__ __launch_bounds__(kScanThreads) void k_plan_items(const int32_t* __re
     }
 }
 
+// Batches of at most kScanThreads sequences: scan, rank and item counting in one
+// workgroup (one thread per sequence, lengths and order kept in LDS), with the
+// same results as k_plan_scan + k_plan_rank + k_plan_items.
+__global__ __launch_bounds__(kScanThreads) void k_plan_small(const int32_t* __restrict__ lengths, int B,
+                                                              int T_expected, int max_len, int H, int64_t qkt_cap,
+                                                              int64_t av_cap, int32_t* __restrict__ tok_off,
+                                                              int64_t* __restrict__ att_off,
+                                                              int32_t* __restrict__ order,
+                                                              int32_t* __restrict__ qkt_item_off,
+                                                              int32_t* __restrict__ av_item_off,
+                                                              int32_t* __restrict__ status) {
+    __shared__ int64_t sh_a[kScanWaves], sh_b[kScanWaves];
+    __shared__ int32_t sL[kScanThreads], sOrder[kScanThreads];
+    __shared__ int sh_flags, sh_max;
+    const int b = threadIdx.x;
+    if (b == 0) {
+        sh_flags = 0;
+        sh_max = 0;
+    }
+    const int L = b < B ? lengths[b] : 0;
+    sL[b] = L;
+    int flags = 0;
+    if (b < B) {
+        if (L < 0) flags |= kDataNegLength;
+        if (L > max_len) flags |= kDataLongLength;
+    }
+    __syncthreads();
+    if (flags) atomicOr(&sh_flags, flags);
+    if (b < B) atomicMax(&sh_max, L);
+    // offsets (negative lengths are flagged and counted as 0)
+    const int64_t Lc = L > 0 ? L : 0;
+    int64_t et, ea, tt, ta;
+    block_exclusive_scan2(Lc, (int64_t)H * Lc * Lc, et, ea, tt, ta, sh_a, sh_b);
+    if (b < B) {
+        tok_off[b] = static_cast<int32_t>(et);
+        att_off[b] = ea;
+    }
+    // longest-first rank (a strict total order: every slot written once)
+    if (b < B) {
+        int rank = 0;
+        for (int k = 0; k < B; ++k) {
+            const int Lk = sL[k];
+            rank += (Lk > L) | ((Lk == L) & (k < b));
+        }
+        sOrder[rank] = b;
+        order[rank] = b;
+    }
+    __syncthreads();
+    int f = sh_flags;
+    if (tt != T_expected) f |= kDataTokenCount;
+    // per-sequence item counts scanned in longest-first order
+    int64_t nq = 0, na = 0;
+    if (b < B && f == 0) {
+        const int64_t nt = (sL[sOrder[b]] + kTile - 1) / kTile;
+        na = (int64_t)H * nt;
+        nq = na * nt;
+    }
+    int64_t eq, ea2, tq, ta2;
+    block_exclusive_scan2(nq, na, eq, ea2, tq, ta2, sh_a, sh_b);
+    if (b < B) {
+        qkt_item_off[b] = static_cast<int32_t>(min(eq, (int64_t)INT_MAX));
+        av_item_off[b] = static_cast<int32_t>(min(ea2, (int64_t)INT_MAX));
+    }
+    if (b == 0) {
+        if (tq > qkt_cap) f |= kDataQktCap;
+        if (ta2 > av_cap) f |= kDataAvCap;
+        tok_off[B] = static_cast<int32_t>(tt);
+        att_off[B] = ta;
+        qkt_item_off[B] = static_cast<int32_t>(min(tq, (int64_t)INT_MAX));
+        av_item_off[B] = static_cast<int32_t>(min(ta2, (int64_t)INT_MAX));
+        status[0] = f;
+        status[1] = f ? 0 : static_cast<int32_t>(tq);
+        status[2] = f ? 0 : static_cast<int32_t>(ta2);
+        status[3] = sh_max;
+    }
+}
+
 // Workgroup k writes the items of the k-th longest sequence and its token map.
 __global__ __launch_bounds__(256) void k_plan_fill(const int32_t* __restrict__ lengths,
                                                     const int32_t* __restrict__ order,
@@ -202,6 +280,14 @@ __global__ __launch_bounds__(256) void k_plan_fill(const int32_t* __restrict__ l
 }  // namespace
 
 hipError_t launch_offsets(const PlanView& p, hipStream_t s) {
+    if (p.batch <= kScanThreads) {
+        hipLaunchKernelGGL(k_plan_small, dim3(1), dim3(kScanThreads), 0, s, p.lengths, p.batch, p.total_tokens,
+                           p.max_len, p.heads, p.qkt_cap, p.av_cap, p.tok_off, p.att_off, p.order, p.qkt_item_off,
+                           p.av_item_off, p.status);
+        hipLaunchKernelGGL(k_plan_fill, dim3(p.batch), dim3(256), 0, s, p.lengths, p.order, p.tok_off, p.heads,
+                           p.qkt_item_off, p.av_item_off, p.qkt_items, p.av_items, p.tok_seq, p.status);
+        return hipGetLastError();
+    }
     hipLaunchKernelGGL(k_plan_scan, dim3(1), dim3(kScanThreads), 0, s, p.lengths, p.batch, p.total_tokens,
                        p.max_len, p.heads, p.tok_off, p.att_off, p.status);
     hipLaunchKernelGGL(k_plan_rank, dim3((p.batch + 255) / 256), dim3(256), 0, s, p.lengths, p.batch, p.order);
