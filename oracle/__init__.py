@@ -49,13 +49,14 @@ def lib():
         p, i32, i64, f64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_double
         l.oracle_offsets.restype = ctypes.c_int
         l.oracle_offsets.argtypes = [i32, p, i32, i32, i32, p, p, p, p, p, p, p, i64, p, i64, p]
-        l.oracle_qkt.argtypes = [ctypes.c_int, i32, p, i32, i32, p, i64, p, i64, f64, p]
-        l.oracle_softmax.argtypes = [ctypes.c_int, i32, p, i32, p, p]
-        l.oracle_attn_v.argtypes = [ctypes.c_int, i32, p, i32, i32, p, p, i64, p, i64]
+        l.oracle_qkt.argtypes = [ctypes.c_int, i32, p, i32, i32, p, i64, p, i64, f64, ctypes.c_int, p]
+        l.oracle_softmax.argtypes = [ctypes.c_int, i32, p, i32, ctypes.c_int, p, p]
+        l.oracle_attn_v.argtypes = [ctypes.c_int, i32, p, i32, i32, ctypes.c_int, p, p, i64, p, i64]
         l.oracle_linear.argtypes = [ctypes.c_int, i64, i32, i32, p, i64, p, p, p, i64, ctypes.c_int, p, i64]
         l.oracle_layernorm.argtypes = [ctypes.c_int, i64, i32, p, i64, p, p, f64, p, i64]
         l.oracle_encoder_layer.restype = ctypes.c_int
-        l.oracle_encoder_layer.argtypes = [ctypes.c_int, i32, p, i32, i32, i32, f64, ctypes.c_int, p, p, p]
+        l.oracle_encoder_layer.argtypes = [ctypes.c_int, i32, p, i32, i32, i32, f64, ctypes.c_int, ctypes.c_int, p, p,
+                                           p]
         l.oracle_round_bf16.argtypes = [i64, p, p]
         _lib = l
     return _lib
@@ -122,28 +123,30 @@ def score_elems(lengths, heads: int) -> int:
     return int(heads * (L * L).sum())
 
 
-def qkt(dtype, lengths, heads, head_dim, q, ldq, k, ldk, scale):
+def qkt(dtype, lengths, heads, head_dim, q, ldq, k, ldk, scale, causal=False):
+    """Scores in the X[b][i][h][j] layout; with `causal` only j <= i is written (the rest stays 0)."""
     L = _lens(lengths)
     S = np.zeros(max(score_elems(L, heads), 1), _storage_dtype(dtype))
     lib().oracle_qkt(_DT[dtype], L.size, _ptr(L), heads, head_dim, _ptr(np.ascontiguousarray(q)), ldq,
-                     _ptr(np.ascontiguousarray(k)), ldk, float(scale), _ptr(S))
+                     _ptr(np.ascontiguousarray(k)), ldk, float(scale), int(causal), _ptr(S))
     return S[:score_elems(L, heads)]
 
 
-def softmax(dtype, lengths, heads, S):
+def softmax(dtype, lengths, heads, S, causal=False):
+    """Row softmax; with `causal` row (b, i, h) covers j <= i only (the rest of P stays 0)."""
     L = _lens(lengths)
     S = np.ascontiguousarray(S)
     P = np.zeros(max(S.size, 1), _storage_dtype(dtype))
-    lib().oracle_softmax(_DT[dtype], L.size, _ptr(L), heads, _ptr(S), _ptr(P))
+    lib().oracle_softmax(_DT[dtype], L.size, _ptr(L), heads, int(causal), _ptr(S), _ptr(P))
     return P[:S.size]
 
 
-def attn_v(dtype, lengths, heads, head_dim, P, v, ldv, ldo=None):
+def attn_v(dtype, lengths, heads, head_dim, P, v, ldv, ldo=None, causal=False):
     L = _lens(lengths)
     T = int(L.sum())
     ldo = heads * head_dim if ldo is None else ldo
     O = np.zeros(max(T * ldo, 1), _storage_dtype(dtype))
-    lib().oracle_attn_v(_DT[dtype], L.size, _ptr(L), heads, head_dim, _ptr(np.ascontiguousarray(P)),
+    lib().oracle_attn_v(_DT[dtype], L.size, _ptr(L), heads, head_dim, int(causal), _ptr(np.ascontiguousarray(P)),
                         _ptr(np.ascontiguousarray(v)), ldv, _ptr(O), ldo)
     return O[:T * ldo].reshape(T, ldo)
 
@@ -174,15 +177,15 @@ def layernorm(dtype, x, gamma, beta, eps=1e-5):
 _WNAMES = ("w_qkv", "b_qkv", "w_o", "b_o", "ln1_g", "ln1_b", "w_ff1", "b_ff1", "w_ff2", "b_ff2", "ln2_g", "ln2_b")
 
 
-def encoder_layer(dtype, lengths, x, weights: dict, d_model, heads, d_ff, eps=1e-5, act=ACT_GELU_ERF):
-    """One post-LN encoder layer over packed tokens x [T, d_model]."""
+def encoder_layer(dtype, lengths, x, weights: dict, d_model, heads, d_ff, eps=1e-5, act=ACT_GELU_ERF, causal=False):
+    """One post-LN encoder layer over packed tokens x [T, d_model] (masked attention with `causal`)."""
     L = _lens(lengths)
     T = int(L.sum())
     arrs = [np.ascontiguousarray(weights[n]) for n in _WNAMES]
     wstruct = (ctypes.c_void_p * 12)(*[a.ctypes.data for a in arrs])
     x = np.ascontiguousarray(x)
     out = np.zeros((max(T, 1), d_model), _storage_dtype(dtype))
-    rc = lib().oracle_encoder_layer(_DT[dtype], L.size, _ptr(L), d_model, heads, d_ff, float(eps), act,
+    rc = lib().oracle_encoder_layer(_DT[dtype], L.size, _ptr(L), d_model, heads, d_ff, float(eps), act, int(causal),
                                     ctypes.cast(wstruct, ctypes.c_void_p), _ptr(x), _ptr(out))
     if rc != 0:
         raise MemoryError("oracle_encoder_layer: allocation failed")

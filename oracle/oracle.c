@@ -207,9 +207,13 @@ int oracle_offsets(int32_t B, const int32_t* L, int32_t H, int32_t tile_m, int32
  *   S[b][i][h][j] = rd(scale * sum_{c < dh} Q[t_i][h*dh + c] * K[t_j][h*dh + c])
  * with t_i = tok_off[b] + i, Q/K packed [T, >= H*dh] with row strides ldq/ldk,
  * and S in the X[b][i][h][j] layout of Section 5.3.
+ * causal != 0 gives masked attention (the decoder's masked MHA, Section 7.2 and
+ * Appendix D): position i sees keys j <= i only, so only the lower triangle
+ * j <= i of each [L_b x L_b] block is computed and written; entries j > i are
+ * left untouched.
  */
 void oracle_qkt(int dtype, int32_t B, const int32_t* L, int32_t H, int32_t dh,
-                const void* q, int64_t ldq, const void* k, int64_t ldk, double scale, void* S) {
+                const void* q, int64_t ldq, const void* k, int64_t ldk, double scale, int causal, void* S) {
     int64_t* tok_off = malloc(sizeof(int64_t) * (B + 1));
     int64_t* att_off = malloc(sizeof(int64_t) * (B + 1));
     token_offsets(B, L, tok_off);
@@ -218,7 +222,7 @@ void oracle_qkt(int dtype, int32_t B, const int32_t* L, int32_t H, int32_t dh,
         int64_t n = L[b];
         for (int64_t i = 0; i < n; ++i)
             for (int32_t h = 0; h < H; ++h)
-                for (int64_t j = 0; j < n; ++j) {
+                for (int64_t j = 0; j < (causal ? i + 1 : n); ++j) {
                     double acc = 0.0;
                     for (int32_t c = 0; c < dh; ++c)
                         acc += load(q, dtype, (tok_off[b] + i) * ldq + (int64_t)h * dh + c) *
@@ -233,9 +237,10 @@ void oracle_qkt(int dtype, int32_t B, const int32_t* L, int32_t H, int32_t dh,
 /*
  * Ragged row softmax (the Softmax operator): every row (b, i, h) of S holds L_b
  * scores; P_j = rd(exp(S_j - m) / sum_k exp(S_k - m)), m = max_k S_k.
- * P may alias S.
+ * P may alias S.  With causal != 0 row (b, i, h) holds the i + 1 scores j <= i
+ * (masked attention); entries j > i are neither read nor written.
  */
-void oracle_softmax(int dtype, int32_t B, const int32_t* L, int32_t H, const void* S, void* P) {
+void oracle_softmax(int dtype, int32_t B, const int32_t* L, int32_t H, int causal, const void* S, void* P) {
     int64_t base = 0;
     double* e = NULL;
     int64_t ecap = 0;
@@ -248,17 +253,18 @@ void oracle_softmax(int dtype, int32_t B, const int32_t* L, int32_t H, const voi
         }
         for (int64_t r = 0; r < n * H; ++r) {
             int64_t row = base + r * n;
+            int64_t len = causal ? r / H + 1 : n;  /* row r is position i = r / H of head r % H */
             double m = -INFINITY;
-            for (int64_t j = 0; j < n; ++j) {
+            for (int64_t j = 0; j < len; ++j) {
                 double s = load(S, dtype, row + j);
                 if (s > m) m = s;
             }
             double sum = 0.0;
-            for (int64_t j = 0; j < n; ++j) {
+            for (int64_t j = 0; j < len; ++j) {
                 e[j] = exp(load(S, dtype, row + j) - m);
                 sum += e[j];
             }
-            for (int64_t j = 0; j < n; ++j) store(P, dtype, row + j, e[j] / sum);
+            for (int64_t j = 0; j < len; ++j) store(P, dtype, row + j, e[j] / sum);
         }
         base += (int64_t)H * n * n;
     }
@@ -268,9 +274,10 @@ void oracle_softmax(int dtype, int32_t B, const int32_t* L, int32_t H, const voi
 /*
  * Ragged Attn.V (the AttnV operator, a reduction over the vloop j):
  *   O[t_i][h*dh + c] = rd(sum_{j < L_b} P[b][i][h][j] * V[t_j][h*dh + c]).
- * O is packed [T, >= H*dh] with row stride ldo.
+ * O is packed [T, >= H*dh] with row stride ldo.  With causal != 0 the sum runs
+ * over j <= i (masked attention).
  */
-void oracle_attn_v(int dtype, int32_t B, const int32_t* L, int32_t H, int32_t dh,
+void oracle_attn_v(int dtype, int32_t B, const int32_t* L, int32_t H, int32_t dh, int causal,
                    const void* P, const void* v, int64_t ldv, void* O, int64_t ldo) {
     int64_t* tok_off = malloc(sizeof(int64_t) * (B + 1));
     int64_t* att_off = malloc(sizeof(int64_t) * (B + 1));
@@ -282,7 +289,7 @@ void oracle_attn_v(int dtype, int32_t B, const int32_t* L, int32_t H, int32_t dh
             for (int32_t h = 0; h < H; ++h)
                 for (int32_t c = 0; c < dh; ++c) {
                     double acc = 0.0;
-                    for (int64_t j = 0; j < n; ++j)
+                    for (int64_t j = 0; j < (causal ? i + 1 : n); ++j)
                         acc += load(P, dtype, att_off[b] + (i * H + h) * n + j) *
                                load(v, dtype, (tok_off[b] + j) * ldv + (int64_t)h * dh + c);
                     store(O, dtype, (tok_off[b] + i) * ldo + (int64_t)h * dh + c, acc);
@@ -381,11 +388,13 @@ static size_t elem_size(int dtype) { return dtype == OR_F32 ? 4 : 2; }
  *   F   = act(H1 W1^T + b1)                   [T, d_ff]
  *   Y2  = F W2^T + b2 + H1
  *   out = LayerNorm2(Y2)
+ * With causal != 0 the attention is masked (position i sees keys j <= i), the
+ * decoder variant of the layer (Section 7.2; Appendix D, masked SDPA).
  * Every intermediate is rounded to the storage type.  Returns 0, or 1 on
  * allocation failure.
  */
 int oracle_encoder_layer(int dtype, int32_t B, const int32_t* L, int32_t d, int32_t H, int32_t d_ff,
-                         double ln_eps, int act, const oracle_layer_weights* w,
+                         double ln_eps, int act, int causal, const oracle_layer_weights* w,
                          const void* x, void* out) {
     int64_t T = 0, S2 = 0;
     for (int32_t b = 0; b < B; ++b) {
@@ -407,9 +416,9 @@ int oracle_encoder_layer(int dtype, int32_t B, const int32_t* L, int32_t d, int3
         goto done;
     }
     oracle_linear(dtype, T, d, 3 * d, x, d, w->w_qkv, w->b_qkv, NULL, 0, OR_ACT_NONE, qkv, 3 * d);
-    oracle_qkt(dtype, B, L, H, dh, qkv, 3 * d, qkv + es * d, 3 * d, 1.0 / sqrt((double)dh), s);
-    oracle_softmax(dtype, B, L, H, s, s);
-    oracle_attn_v(dtype, B, L, H, dh, s, qkv + es * 2 * d, 3 * d, o, d);
+    oracle_qkt(dtype, B, L, H, dh, qkv, 3 * d, qkv + es * d, 3 * d, 1.0 / sqrt((double)dh), causal, s);
+    oracle_softmax(dtype, B, L, H, causal, s, s);
+    oracle_attn_v(dtype, B, L, H, dh, causal, s, qkv + es * 2 * d, 3 * d, o, d);
     oracle_linear(dtype, T, d, d, o, d, w->w_o, w->b_o, x, d, OR_ACT_NONE, y1, d);
     oracle_layernorm(dtype, T, d, y1, d, w->ln1_g, w->ln1_b, ln_eps, h1, d);
     oracle_linear(dtype, T, d, d_ff, h1, d, w->w_ff1, w->b_ff1, NULL, 0, act, f, d_ff);
