@@ -16,6 +16,7 @@ from __future__ import annotations
 import argparse
 import ctypes
 import hashlib
+import math
 import json
 import os
 import sys
@@ -200,6 +201,45 @@ def derive_traffic(fetch_csv, write_csv, cal_fetch_csv, cal_write_csv, copy_mib)
     print(json.dumps(out, indent=1, sort_keys=True))
 
 
+def masked_measurement(rag, plan, wl, x, wstruct, ws, y, flags, iters=20):
+    """Masked (causal) attention on the same batch: the fused kernel with and without the
+    mask on packed Q, K, V of the layer's shape, and the masked layer.  Useful FLOPs of
+    masked attention count the lower triangles only: 2 * d * sum L (L + 1)."""
+    import torch
+
+    cfg = wl.cfg
+    L = wl.lengths.astype(np.float64)
+    T, d, dff = wl.total_tokens, cfg.d_model, cfg.d_ff
+    g = torch.Generator(device="cuda").manual_seed(1)
+    q, k, v = (torch.randn(T, d, device="cuda", generator=g).bfloat16() for _ in range(3))
+    o = torch.empty(T, d, device="cuda", dtype=torch.bfloat16)
+    scale = 1.0 / math.sqrt(64)
+
+    def timed(fn):
+        for _ in range(3):
+            fn()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(iters):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / iters
+
+    rag.ragged_offsets(plan)
+    ms_full = timed(lambda: rag.ragged_attention(plan, q, k, v, o, scale))
+    ms_mask = timed(lambda: rag.ragged_attention_causal(plan, q, k, v, o, scale))
+    ms_layer = timed(lambda: rag.encoder_layer(plan, x, y, wstruct, dff, ws, flags=flags | rag.RAG_LAYER_CAUSAL))
+    assert not plan.data_errors(), plan.data_errors()
+    fl_mask = 2.0 * d * float((L * (L + 1)).sum())
+    fl_layer = 2.0 * T * d * (4 * d + 2 * dff) + fl_mask
+    return {"attention_ms": round(ms_mask, 4), "attention_unmasked_ms": round(ms_full, 4),
+            "speedup_vs_unmasked": round(ms_full / ms_mask, 3),
+            "attention_useful_tflops": round(fl_mask / (ms_mask * 1e-3) / 1e12, 1),
+            "layer_ms": round(ms_layer, 4), "layer_useful_tflops": round(fl_layer / (ms_layer * 1e-3) / 1e12, 1),
+            "note": "fused causal attention and the masked layer (plan included once, not per call)"}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -209,6 +249,7 @@ def main():
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--flags", type=int, default=0, help="encoder_layer flags (1 = unfused attention)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-masked", action="store_true", help="skip the masked (causal) attention measurement")
     ap.add_argument("--cpu-target-flops", type=float, default=2.0e10)
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of MIB MiB five times (counter calibration) and exit")
@@ -353,6 +394,8 @@ def main():
         "stage_ms": {**{"prelude": round(prelude_ms, 4)}, **{s: round(v, 4) for s, v in stage_ms.items()}},
         "roofline": roof,
     }
+    if not args.no_masked:
+        out["masked"] = masked_measurement(rag, plan, wl, x, wstruct, ws, y, args.flags)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(wl, args.cpu_target_flops)
     else:

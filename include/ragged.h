@@ -197,14 +197,42 @@ rag_status ragged_attn_v(const rag_plan* plan, const void* probs, int64_t score_
  * Fused ragged attention (bf16, plan max_len <= RAG_FUSED_MAX_LEN): the
  * composition of ragged_qkt, ragged_softmax and ragged_attn_v,
  *   out[t_i][h*hd + c] = sum_j softmax_j(scale * q_i . k_j) v[t_j][h*hd + c],
- * computed per (sequence, head, 64-query-row) item with the same rounding
- * points (bf16 scores, exact softmax over the whole row, bf16 probabilities)
- * while the scores stay in registers, so none reaches memory.  Same operand
- * rules as the three operators; RAG_ERR_SHAPE if max_len is too long.
+ * computed per (sequence, head) in one pass over the keys without storing
+ * scores or probabilities: fp32 scores, an online softmax, bf16 unnormalised
+ * exponentials as the operand of the P.V product and one division by the row
+ * sum (so it differs from the three operators by rounding only).  Same operand
+ * rules as the three operators; RAG_ERR_DTYPE unless bf16, RAG_ERR_SHAPE if
+ * max_len is too long.
  */
 rag_status ragged_attention(const rag_plan* plan, const void* q, int32_t ldq, const void* k, int32_t ldk,
                             const void* v, int32_t ldv, int32_t head_dim, float scale, void* out,
                             int32_t ldo, int32_t dtype, void* stream);
+
+/*
+ * Masked (causal) attention, the decoder's masked MHA (Section 7.2; Appendix D,
+ * masked SDPA): position i attends to keys j <= i only, so each sequence's
+ * attention matrix is lower triangular.  Same arguments, layout and errors as
+ * the unmasked calls above, with these differences:
+ *   ragged_qkt_causal      writes only the entries j <= i of each [L_b x L_b]
+ *                          block (tiles above the diagonal are skipped; the
+ *                          upper triangle of `scores` is left untouched);
+ *   ragged_softmax_causal  row (b, i, h) covers its i + 1 scores j <= i, and
+ *                          only those entries of `probs` are written;
+ *   ragged_attn_v_causal   sums over j <= i (entries j > i of `probs` are not
+ *                          read);
+ *   ragged_attention_causal  the fused path, walking keys up to each query.
+ */
+rag_status ragged_qkt_causal(const rag_plan* plan, const void* q, int32_t ldq, const void* k, int32_t ldk,
+                             int32_t head_dim, float scale, void* scores, int64_t score_cap,
+                             int32_t dtype, void* stream);
+rag_status ragged_softmax_causal(const rag_plan* plan, const void* scores, void* probs, int64_t score_cap,
+                                 int32_t dtype, void* stream);
+rag_status ragged_attn_v_causal(const rag_plan* plan, const void* probs, int64_t score_cap, const void* v,
+                                int32_t ldv, int32_t head_dim, void* out, int32_t ldo, int32_t dtype,
+                                void* stream);
+rag_status ragged_attention_causal(const rag_plan* plan, const void* q, int32_t ldq, const void* k,
+                                   int32_t ldk, const void* v, int32_t ldv, int32_t head_dim, float scale,
+                                   void* out, int32_t ldo, int32_t dtype, void* stream);
 
 /*
  * Packed-token linear operator (Proj1 / Proj2 / FF1 / FF2 of the layer, run
@@ -231,8 +259,10 @@ rag_status packed_layernorm(const void* x, int32_t ldx, const void* gamma, const
 
 /* encoder_layer flags */
 enum {
-    RAG_LAYER_UNFUSED_ATTENTION = 1 /* run ragged_qkt/softmax/attn_v with a
-                                       materialised score buffer in the workspace */
+    RAG_LAYER_UNFUSED_ATTENTION = 1, /* run ragged_qkt/softmax/attn_v with a
+                                        materialised score buffer in the workspace */
+    RAG_LAYER_CAUSAL = 2             /* masked attention (position i sees keys j <= i):
+                                        the decoder variant of the layer */
 };
 
 /* Number of events encoder_layer records when `events` is not NULL. */

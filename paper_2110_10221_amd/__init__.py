@@ -26,6 +26,7 @@ RAG_ACT_NONE, RAG_ACT_GELU_ERF, RAG_ACT_GELU_TANH = 0, 1, 2
 RAG_TILE = 64
 RAG_HEAD_DIM = 64
 RAG_LAYER_UNFUSED_ATTENTION = 1
+RAG_LAYER_CAUSAL = 2
 RAG_LAYER_EVENTS = 10
 DATA_BITS = {1: "negative length", 2: "length > max_len", 4: "sum of lengths != total_tokens",
              8: "qkt_cap exceeded", 16: "av_cap exceeded", 32: "score buffer too small"}
@@ -70,6 +71,10 @@ _c_softmax = _sig("ragged_softmax", [ctypes.POINTER(RagPlan), _p, _p, _i64, _i32
 _c_attn_v = _sig("ragged_attn_v", [ctypes.POINTER(RagPlan), _p, _i64, _p, _i32, _i32, _p, _i32, _i32, _p])
 _c_attention = _sig("ragged_attention", [ctypes.POINTER(RagPlan), _p, _i32, _p, _i32, _p, _i32, _i32, _f32, _p,
                                          _i32, _i32, _p])
+_c_qkt_causal = _sig("ragged_qkt_causal", list(_c_qkt.argtypes))
+_c_softmax_causal = _sig("ragged_softmax_causal", list(_c_softmax.argtypes))
+_c_attn_v_causal = _sig("ragged_attn_v_causal", list(_c_attn_v.argtypes))
+_c_attention_causal = _sig("ragged_attention_causal", list(_c_attention.argtypes))
 _c_linear = _sig("packed_linear", [_p, _i32, _p, _p, _p, _i32, _i32, _p, _i32, _i32, _i32, _i32, _i32, _p])
 _c_layernorm = _sig("packed_layernorm", [_p, _i32, _p, _p, _f32, _p, _i32, _i32, _i32, _i32, _p])
 _c_ws = _sig("encoder_layer_workspace", [_i32, _i32, _i32, _i32, _i32, _i32, _i32, ctypes.POINTER(ctypes.c_size_t)])
@@ -175,10 +180,23 @@ def ragged_qkt(plan: Plan, q, k, scores, scale, head_dim=RAG_HEAD_DIM, stream=No
                                 scores.numel(), _dtype_code(q), _stream(stream)))
 
 
+def ragged_qkt_causal(plan: Plan, q, k, scores, scale, head_dim=RAG_HEAD_DIM, stream=None):
+    _check("ragged_qkt_causal", _c_qkt_causal(plan.ref(), _ptr(q), _ld(q), _ptr(k), _ld(k), head_dim, scale,
+                                              _ptr(scores), scores.numel(), _dtype_code(q), _stream(stream)))
+
+
 def ragged_softmax(plan: Plan, scores, probs=None, stream=None):
     probs = scores if probs is None else probs
     _check("ragged_softmax", _c_softmax(plan.ref(), _ptr(scores), _ptr(probs), min(scores.numel(), probs.numel()),
                                         _dtype_code(scores), _stream(stream)))
+    return probs
+
+
+def ragged_softmax_causal(plan: Plan, scores, probs=None, stream=None):
+    probs = scores if probs is None else probs
+    _check("ragged_softmax_causal", _c_softmax_causal(plan.ref(), _ptr(scores), _ptr(probs),
+                                                      min(scores.numel(), probs.numel()), _dtype_code(scores),
+                                                      _stream(stream)))
     return probs
 
 
@@ -187,9 +205,20 @@ def ragged_attn_v(plan: Plan, probs, v, out, head_dim=RAG_HEAD_DIM, stream=None)
                                       _ld(out), _dtype_code(v), _stream(stream)))
 
 
+def ragged_attn_v_causal(plan: Plan, probs, v, out, head_dim=RAG_HEAD_DIM, stream=None):
+    _check("ragged_attn_v_causal", _c_attn_v_causal(plan.ref(), _ptr(probs), probs.numel(), _ptr(v), _ld(v),
+                                                    head_dim, _ptr(out), _ld(out), _dtype_code(v), _stream(stream)))
+
+
 def ragged_attention(plan: Plan, q, k, v, out, scale, head_dim=RAG_HEAD_DIM, stream=None):
     _check("ragged_attention", _c_attention(plan.ref(), _ptr(q), _ld(q), _ptr(k), _ld(k), _ptr(v), _ld(v), head_dim,
                                             scale, _ptr(out), _ld(out), _dtype_code(q), _stream(stream)))
+
+
+def ragged_attention_causal(plan: Plan, q, k, v, out, scale, head_dim=RAG_HEAD_DIM, stream=None):
+    _check("ragged_attention_causal", _c_attention_causal(plan.ref(), _ptr(q), _ld(q), _ptr(k), _ld(k), _ptr(v),
+                                                          _ld(v), head_dim, scale, _ptr(out), _ld(out),
+                                                          _dtype_code(q), _stream(stream)))
 
 
 def packed_linear(x, w, y, bias=None, residual=None, act=RAG_ACT_NONE, stream=None):

@@ -170,10 +170,11 @@ rag_status ragged_offsets(rag_plan* plan, void* stream) {
     return finish(rag::launch_offsets(v, s), s, plan->status, fn);
 }
 
-rag_status ragged_qkt(const rag_plan* plan, const void* q, int32_t ldq, const void* k, int32_t ldk,
-                      int32_t head_dim, float scale, void* scores, int64_t score_cap, int32_t dtype,
-                      void* stream) {
-    const char* fn = "ragged_qkt";
+namespace {
+
+rag_status qkt_impl(const rag_plan* plan, const void* q, int32_t ldq, const void* k, int32_t ldk, int32_t head_dim,
+                    float scale, void* scores, int64_t score_cap, int32_t dtype, void* stream, bool causal,
+                    const char* fn) {
     rag::PlanView v;
     rag_status st;
     if ((st = view_plan(plan, v, fn)) || (st = check_dtype(dtype, fn))) return st;
@@ -184,12 +185,11 @@ rag_status ragged_qkt(const rag_plan* plan, const void* q, int32_t ldq, const vo
     if (!scores || score_cap < 0) return fail(RAG_ERR_ARG, "%s: scores is NULL or score_cap < 0", fn);
     if (!aligned(scores, elem_size(dtype))) return fail(RAG_ERR_ARG, "%s: scores misaligned", fn);
     hipStream_t s = static_cast<hipStream_t>(stream);
-    return finish(rag::launch_qkt(v, dtype, q, ldq, k, ldk, scale, scores, score_cap, s), s, plan->status, fn);
+    return finish(rag::launch_qkt(v, dtype, q, ldq, k, ldk, scale, scores, score_cap, causal, s), s, plan->status, fn);
 }
 
-rag_status ragged_softmax(const rag_plan* plan, const void* scores, void* probs, int64_t score_cap, int32_t dtype,
-                          void* stream) {
-    const char* fn = "ragged_softmax";
+rag_status softmax_impl(const rag_plan* plan, const void* scores, void* probs, int64_t score_cap, int32_t dtype,
+                        void* stream, bool causal, const char* fn) {
     rag::PlanView v;
     rag_status st;
     if ((st = view_plan(plan, v, fn)) || (st = check_dtype(dtype, fn))) return st;
@@ -197,12 +197,12 @@ rag_status ragged_softmax(const rag_plan* plan, const void* scores, void* probs,
     if (!aligned(scores, elem_size(dtype)) || !aligned(probs, elem_size(dtype)))
         return fail(RAG_ERR_ARG, "%s: scores/probs misaligned", fn);
     hipStream_t s = static_cast<hipStream_t>(stream);
-    return finish(rag::launch_softmax(v, dtype, scores, probs, score_cap, s), s, plan->status, fn);
+    return finish(rag::launch_softmax(v, dtype, scores, probs, score_cap, causal, s), s, plan->status, fn);
 }
 
-rag_status ragged_attn_v(const rag_plan* plan, const void* probs, int64_t score_cap, const void* vv, int32_t ldv,
-                         int32_t head_dim, void* out, int32_t ldo, int32_t dtype, void* stream) {
-    const char* fn = "ragged_attn_v";
+rag_status attn_v_impl(const rag_plan* plan, const void* probs, int64_t score_cap, const void* vv, int32_t ldv,
+                       int32_t head_dim, void* out, int32_t ldo, int32_t dtype, void* stream, bool causal,
+                       const char* fn) {
     rag::PlanView v;
     rag_status st;
     if ((st = view_plan(plan, v, fn)) || (st = check_dtype(dtype, fn))) return st;
@@ -213,13 +213,12 @@ rag_status ragged_attn_v(const rag_plan* plan, const void* probs, int64_t score_
     if (!probs || score_cap < 0) return fail(RAG_ERR_ARG, "%s: probs is NULL or score_cap < 0", fn);
     if (!aligned(probs, elem_size(dtype))) return fail(RAG_ERR_ARG, "%s: probs misaligned", fn);
     hipStream_t s = static_cast<hipStream_t>(stream);
-    return finish(rag::launch_attn_v(v, dtype, probs, score_cap, vv, ldv, out, ldo, s), s, plan->status, fn);
+    return finish(rag::launch_attn_v(v, dtype, probs, score_cap, vv, ldv, out, ldo, causal, s), s, plan->status, fn);
 }
 
-rag_status ragged_attention(const rag_plan* plan, const void* q, int32_t ldq, const void* k, int32_t ldk,
-                            const void* vv, int32_t ldv, int32_t head_dim, float scale, void* out, int32_t ldo,
-                            int32_t dtype, void* stream) {
-    const char* fn = "ragged_attention";
+rag_status attention_impl(const rag_plan* plan, const void* q, int32_t ldq, const void* k, int32_t ldk,
+                          const void* vv, int32_t ldv, int32_t head_dim, float scale, void* out, int32_t ldo,
+                          int32_t dtype, void* stream, bool causal, const char* fn) {
     rag::PlanView v;
     rag_status st;
     if ((st = view_plan(plan, v, fn)) || (st = check_dtype(dtype, fn))) return st;
@@ -232,7 +231,59 @@ rag_status ragged_attention(const rag_plan* plan, const void* q, int32_t ldq, co
         (st = check_operand(vv, ldv, width, dtype, 16, "v", fn)) || (st = check_operand(out, ldo, width, dtype, 16, "out", fn)))
         return st;
     hipStream_t s = static_cast<hipStream_t>(stream);
-    return finish(rag::launch_fused_attention(v, dtype, q, ldq, k, ldk, vv, ldv, scale, out, ldo, s), s, plan->status, fn);
+    return finish(rag::launch_fused_attention(v, dtype, q, ldq, k, ldk, vv, ldv, scale, out, ldo, causal, s), s,
+                  plan->status, fn);
+}
+
+}  // namespace
+
+rag_status ragged_qkt(const rag_plan* plan, const void* q, int32_t ldq, const void* k, int32_t ldk,
+                      int32_t head_dim, float scale, void* scores, int64_t score_cap, int32_t dtype,
+                      void* stream) {
+    return qkt_impl(plan, q, ldq, k, ldk, head_dim, scale, scores, score_cap, dtype, stream, false, "ragged_qkt");
+}
+
+rag_status ragged_qkt_causal(const rag_plan* plan, const void* q, int32_t ldq, const void* k, int32_t ldk,
+                             int32_t head_dim, float scale, void* scores, int64_t score_cap, int32_t dtype,
+                             void* stream) {
+    return qkt_impl(plan, q, ldq, k, ldk, head_dim, scale, scores, score_cap, dtype, stream, true,
+                    "ragged_qkt_causal");
+}
+
+rag_status ragged_softmax(const rag_plan* plan, const void* scores, void* probs, int64_t score_cap, int32_t dtype,
+                          void* stream) {
+    return softmax_impl(plan, scores, probs, score_cap, dtype, stream, false, "ragged_softmax");
+}
+
+rag_status ragged_softmax_causal(const rag_plan* plan, const void* scores, void* probs, int64_t score_cap,
+                                 int32_t dtype, void* stream) {
+    return softmax_impl(plan, scores, probs, score_cap, dtype, stream, true, "ragged_softmax_causal");
+}
+
+rag_status ragged_attn_v(const rag_plan* plan, const void* probs, int64_t score_cap, const void* vv, int32_t ldv,
+                         int32_t head_dim, void* out, int32_t ldo, int32_t dtype, void* stream) {
+    return attn_v_impl(plan, probs, score_cap, vv, ldv, head_dim, out, ldo, dtype, stream, false, "ragged_attn_v");
+}
+
+rag_status ragged_attn_v_causal(const rag_plan* plan, const void* probs, int64_t score_cap, const void* vv,
+                                int32_t ldv, int32_t head_dim, void* out, int32_t ldo, int32_t dtype,
+                                void* stream) {
+    return attn_v_impl(plan, probs, score_cap, vv, ldv, head_dim, out, ldo, dtype, stream, true,
+                       "ragged_attn_v_causal");
+}
+
+rag_status ragged_attention(const rag_plan* plan, const void* q, int32_t ldq, const void* k, int32_t ldk,
+                            const void* vv, int32_t ldv, int32_t head_dim, float scale, void* out, int32_t ldo,
+                            int32_t dtype, void* stream) {
+    return attention_impl(plan, q, ldq, k, ldk, vv, ldv, head_dim, scale, out, ldo, dtype, stream, false,
+                          "ragged_attention");
+}
+
+rag_status ragged_attention_causal(const rag_plan* plan, const void* q, int32_t ldq, const void* k, int32_t ldk,
+                                   const void* vv, int32_t ldv, int32_t head_dim, float scale, void* out,
+                                   int32_t ldo, int32_t dtype, void* stream) {
+    return attention_impl(plan, q, ldq, k, ldk, vv, ldv, head_dim, scale, out, ldo, dtype, stream, true,
+                          "ragged_attention_causal");
 }
 
 namespace {
@@ -356,7 +407,7 @@ rag_status encoder_layer(const rag_plan* plan, const void* x, void* y, int32_t d
     if (heads != plan->heads) return fail(RAG_ERR_SHAPE, "%s: heads %d differs from the plan's %d", fn, heads, plan->heads);
     if (head_dim != RAG_HEAD_DIM) return fail(RAG_ERR_SHAPE, "%s: head_dim %d unsupported (only %d)", fn, head_dim, RAG_HEAD_DIM);
     if (d_model != heads * head_dim) return fail(RAG_ERR_SHAPE, "%s: d_model %d != heads * head_dim", fn, d_model);
-    if (flags & ~RAG_LAYER_UNFUSED_ATTENTION) return fail(RAG_ERR_ARG, "%s: unknown flags 0x%x", fn, flags);
+    if (flags & ~(RAG_LAYER_UNFUSED_ATTENTION | RAG_LAYER_CAUSAL)) return fail(RAG_ERR_ARG, "%s: unknown flags 0x%x", fn, flags);
     const int T = plan->total_tokens, d = d_model;
     const LayerBuffers lb = layer_buffers(T, plan->max_len, d, heads, d_ff, dtype, flags);
     if (!workspace || workspace_bytes < lb.total)
@@ -392,21 +443,22 @@ rag_status encoder_layer(const rag_plan* plan, const void* x, void* y, int32_t d
         if (e == hipSuccess) e = r;
     };
     const float scale = 1.0f / sqrtf((float)head_dim);
+    const bool causal = (flags & RAG_LAYER_CAUSAL) != 0;
     mark(0);
     run(rag::launch_linear(dtype, x, d, w->w_qkv, w->b_qkv, nullptr, 0, RAG_ACT_NONE, qkv, 3 * d, T, d, 3 * d, s));
     mark(1);
     if (unfused_attention(dtype, flags, plan->max_len)) {
         const int64_t cap = (int64_t)(lb.scores / es);
-        run(rag::launch_qkt(v, dtype, qkvc, 3 * d, qkvc + es * d, 3 * d, scale, scores, cap, s));
+        run(rag::launch_qkt(v, dtype, qkvc, 3 * d, qkvc + es * d, 3 * d, scale, scores, cap, causal, s));
         mark(2);
-        run(rag::launch_softmax(v, dtype, scores, scores, cap, s));
+        run(rag::launch_softmax(v, dtype, scores, scores, cap, causal, s));
         mark(3);
-        run(rag::launch_attn_v(v, dtype, scores, cap, qkvc + 2 * es * d, 3 * d, h1o, d, s));
+        run(rag::launch_attn_v(v, dtype, scores, cap, qkvc + 2 * es * d, 3 * d, h1o, d, causal, s));
     } else {
         mark(2);
         mark(3);
         run(rag::launch_fused_attention(v, dtype, qkvc, 3 * d, qkvc + es * d, 3 * d, qkvc + 2 * es * d, 3 * d, scale,
-                                        h1o, d, s));
+                                        h1o, d, causal, s));
     }
     mark(4);
     run(rag::launch_linear(dtype, h1o, d, w->w_o, w->b_o, x, d, RAG_ACT_NONE, act_a, d, T, d, d, s));

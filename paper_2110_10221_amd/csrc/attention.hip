@@ -58,7 +58,7 @@ constexpr int kStage = kTile + 8;  // padded LDS row (elements)
 
 __global__ __launch_bounds__(256) void k_qkt_bf16(PlanArgs pa, const uint16_t* __restrict__ q, int ldq,
                                                    const uint16_t* __restrict__ k, int ldk, float scale,
-                                                   uint16_t* __restrict__ S, int64_t score_cap) {
+                                                   uint16_t* __restrict__ S, int64_t score_cap, int causal) {
     if (!plan_ok(pa, score_cap)) return;
     __shared__ uint16_t tile[kTile][kStage];
     const int n_items = pa.status[1];
@@ -68,6 +68,7 @@ __global__ __launch_bounds__(256) void k_qkt_bf16(PlanArgs pa, const uint16_t* _
     for (int it = blockIdx.x; it < n_items; it += gridDim.x) {
         const int4 item = reinterpret_cast<const int4*>(pa.qkt_items)[it];
         const int b = item.x, h = item.y, ti = item.z, tj = item.w;
+        if (causal && tj > ti) continue;  // masked: tiles above the diagonal hold no score
         const int L = pa.lengths[b];
         const int t0 = pa.tok_off[b];
         const int64_t base = pa.att_off[b];
@@ -93,15 +94,17 @@ __global__ __launch_bounds__(256) void k_qkt_bf16(PlanArgs pa, const uint16_t* _
                 tile[wave * 16 + l16][jb * 16 + 4 * q4 + r] = f32_to_bf16(acc[jb][r] * scale);
         __syncthreads();
         const int rows = min(kTile, L - ti * kTile), cols = min(kTile, L - tj * kTile);
+        // masked: only keys j <= i are written (the diagonal tile's upper part is left alone)
+        const int jmax = causal ? ti * kTile - tj * kTile : kTile;
         for (int rr = wave; rr < rows; rr += 4)
-            if (lane < cols)
+            if (lane < cols && lane <= jmax + rr)
                 S[base + ((int64_t)(ti * kTile + rr) * H + h) * L + tj * kTile + lane] = tile[rr][lane];
     }
 }
 
 __global__ __launch_bounds__(256) void k_qkt_f32(PlanArgs pa, const float* __restrict__ q, int ldq,
                                                   const float* __restrict__ k, int ldk, float scale,
-                                                  float* __restrict__ S, int64_t score_cap) {
+                                                  float* __restrict__ S, int64_t score_cap, int causal) {
     if (!plan_ok(pa, score_cap)) return;
     __shared__ float Qs[kTile][kHeadDim + 1], Ks[kTile][kHeadDim + 1];
     const int n_items = pa.status[1];
@@ -110,6 +113,7 @@ __global__ __launch_bounds__(256) void k_qkt_f32(PlanArgs pa, const float* __res
     for (int it = blockIdx.x; it < n_items; it += gridDim.x) {
         const int4 item = reinterpret_cast<const int4*>(pa.qkt_items)[it];
         const int b = item.x, h = item.y, ti = item.z, tj = item.w;
+        if (causal && tj > ti) continue;
         const int L = pa.lengths[b];
         const int t0 = pa.tok_off[b];
         const int64_t base = pa.att_off[b];
@@ -142,7 +146,8 @@ __global__ __launch_bounds__(256) void k_qkt_f32(PlanArgs pa, const float* __res
 #pragma unroll
             for (int v = 0; v < 4; ++v) {
                 const int j = tx + 16 * v;
-                if (j < cols) S[base + ((int64_t)(ti * kTile + i) * H + h) * L + tj * kTile + j] = acc[u][v] * scale;
+                if (j < cols && (!causal || tj * kTile + j <= ti * kTile + i))
+                    S[base + ((int64_t)(ti * kTile + i) * H + h) * L + tj * kTile + j] = acc[u][v] * scale;
             }
         }
     }
@@ -173,16 +178,18 @@ constexpr int kSoftmaxRegs = 8;  // rows up to 64 * 8 = 512 scores stay in regis
 
 template <bool BF16>
 __global__ __launch_bounds__(256) void k_softmax(PlanArgs pa, const typename Elem<BF16>::T* S,
-                                                  typename Elem<BF16>::T* P, int64_t score_cap, int T) {
+                                                  typename Elem<BF16>::T* P, int64_t score_cap, int T, int causal) {
     using E = Elem<BF16>;
     if (!plan_ok(pa, score_cap)) return;
     const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
     const int t = blockIdx.x * 4 + wave;
     if (t >= T) return;
     const int b = pa.tok_seq[t];
-    const int L = pa.lengths[b];
     const int H = pa.heads;
-    const int64_t row0 = pa.att_off[b] + (int64_t)(t - pa.tok_off[b]) * H * L;
+    const int ld = pa.lengths[b];                 // row stride: the sequence length
+    const int pos = t - pa.tok_off[b];
+    const int L = causal ? pos + 1 : ld;          // scores in each of this token's rows
+    const int64_t row0 = pa.att_off[b] + (int64_t)pos * H * ld;
     if (L <= kWave) {
         // 64/G rows per pass, G = next power of two >= L lanes per row
         int G = 1;
@@ -191,7 +198,7 @@ __global__ __launch_bounds__(256) void k_softmax(PlanArgs pa, const typename Ele
         for (int h0 = 0; h0 < H; h0 += R) {
             const int h = h0 + r;
             const bool valid = (h < H) && (e < L);
-            const int64_t off = row0 + (int64_t)h * L + e;
+            const int64_t off = row0 + (int64_t)h * ld + e;
             const float x = valid ? E::load(S + off) : -FLT_MAX;
             const float m = group_max(x, G);
             const float ex = valid ? E::exp(x - m) : 0.f;
@@ -200,7 +207,7 @@ __global__ __launch_bounds__(256) void k_softmax(PlanArgs pa, const typename Ele
         }
     } else if (L <= kWave * kSoftmaxRegs) {
         for (int h = 0; h < H; ++h) {
-            const int64_t rp = row0 + (int64_t)h * L;
+            const int64_t rp = row0 + (int64_t)h * ld;
             float x[kSoftmaxRegs];
             float m = -FLT_MAX;
 #pragma unroll
@@ -228,7 +235,7 @@ __global__ __launch_bounds__(256) void k_softmax(PlanArgs pa, const typename Ele
         // long rows: max pass, sum pass, write pass (each element is read before
         // the same lane overwrites it, so in-place use is safe)
         for (int h = 0; h < H; ++h) {
-            const int64_t rp = row0 + (int64_t)h * L;
+            const int64_t rp = row0 + (int64_t)h * ld;
             float m = -FLT_MAX;
             for (int j = lane; j < L; j += kWave) m = fmaxf(m, E::load(S + rp + j));
             m = wave_max(m);
@@ -246,7 +253,7 @@ __global__ __launch_bounds__(256) void k_softmax(PlanArgs pa, const typename Ele
 
 __global__ __launch_bounds__(256) void k_attn_v_bf16(PlanArgs pa, const uint16_t* __restrict__ P,
                                                       int64_t score_cap, const uint16_t* __restrict__ v,
-                                                      int ldv, uint16_t* __restrict__ O, int ldo) {
+                                                      int ldv, uint16_t* __restrict__ O, int ldo, int causal) {
     if (!plan_ok(pa, score_cap)) return;
     __shared__ __attribute__((aligned(16))) uint16_t Ps[kTile][kStage];  // [i][j]
     __shared__ __attribute__((aligned(16))) uint16_t Vt[kTile][kStage];  // [c][j]
@@ -263,15 +270,17 @@ __global__ __launch_bounds__(256) void k_attn_v_bf16(PlanArgs pa, const uint16_t
         floatx4 acc[4];
 #pragma unroll
         for (int cb = 0; cb < 4; ++cb) acc[cb] = floatx4{0.f, 0.f, 0.f, 0.f};
-        for (int j0 = 0; j0 < L; j0 += kTile) {
+        const int jend = causal ? min(L, (ti + 1) * kTile) : L;  // masked: keys up to the diagonal tile
+        for (int j0 = 0; j0 < jend; j0 += kTile) {
             const int cols = min(kTile, L - j0);
             __syncthreads();
-            // probabilities: rows i of the tile, keys j0..j0+63 (zero outside)
+            // probabilities: rows i of the tile, keys j0..j0+63 (zero outside, and above the diagonal when masked)
 #pragma unroll 4
             for (int r = 0; r < 16; ++r) {
                 const int i = threadIdx.x / kWave + 4 * r, j = lane;
                 uint16_t val = 0;
-                if (i < rows && j < cols) val = P[base + ((int64_t)(ti * kTile + i) * H + h) * L + j0 + j];
+                if (i < rows && j < cols && (!causal || j0 + j <= ti * kTile + i))
+                    val = P[base + ((int64_t)(ti * kTile + i) * H + h) * L + j0 + j];
                 Ps[i][j] = val;
             }
             // values: 64 keys x 64 channels, stored transposed [c][j]
@@ -312,7 +321,7 @@ __global__ __launch_bounds__(256) void k_attn_v_bf16(PlanArgs pa, const uint16_t
 
 __global__ __launch_bounds__(256) void k_attn_v_f32(PlanArgs pa, const float* __restrict__ P, int64_t score_cap,
                                                      const float* __restrict__ v, int ldv, float* __restrict__ O,
-                                                     int ldo) {
+                                                     int ldo, int causal) {
     if (!plan_ok(pa, score_cap)) return;
     __shared__ float Ps[kTile][kTile + 1], Vs[kTile][kHeadDim + 1];
     const int n_items = pa.status[2];
@@ -325,12 +334,15 @@ __global__ __launch_bounds__(256) void k_attn_v_f32(PlanArgs pa, const float* __
         const int64_t base = pa.att_off[b];
         const int rows = min(kTile, L - ti * kTile);
         float acc[4][4] = {};
-        for (int j0 = 0; j0 < L; j0 += kTile) {
+        const int jend = causal ? min(L, (ti + 1) * kTile) : L;
+        for (int j0 = 0; j0 < jend; j0 += kTile) {
             const int cols = min(kTile, L - j0);
             __syncthreads();
             for (int e = threadIdx.x; e < kTile * kTile; e += 256) {
                 const int r = e / kTile, c = e % kTile;
-                Ps[r][c] = (r < rows && c < cols) ? P[base + ((int64_t)(ti * kTile + r) * H + h) * L + j0 + c] : 0.f;
+                Ps[r][c] = (r < rows && c < cols && (!causal || j0 + c <= ti * kTile + r))
+                               ? P[base + ((int64_t)(ti * kTile + r) * H + h) * L + j0 + c]
+                               : 0.f;
                 Vs[r][c] = r < cols ? v[(int64_t)(t0 + j0 + r) * ldv + h * kHeadDim + c] : 0.f;
             }
             __syncthreads();
@@ -421,6 +433,16 @@ __device__ __forceinline__ float sum_xor32(float v) {
     return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
+// Masked attention: query block qb (32 rows) needs key chunks 0..qb only, so block
+// qb costs qb + 1 chunks.  Waves w and w + 4k share SIMD w % 4; blocks are dealt to
+// waves in a snake (SIMDs 0,1,2,3 then 3,2,1,0, ...) so every SIMD gets the same
+// number of chunks when a sequence has 16 blocks.
+__device__ __forceinline__ int snake_block(int wave) {
+    const int g = wave / 4, s = wave % 4;
+    return 4 * g + ((g & 1) ? 3 - s : s);
+}
+
+template <bool CAUSAL>
 __global__ __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(kAttnWaves / 4, kAttnWaves / 4)))
 void k_attention_bf16(PlanArgs pa, const int32_t* __restrict__ order, const uint16_t* __restrict__ q, int ldq,
                       const uint16_t* __restrict__ k, int ldk, const uint16_t* __restrict__ v, int ldv, float scale,
@@ -471,8 +493,9 @@ void k_attention_bf16(PlanArgs pa, const int32_t* __restrict__ order, const uint
 #pragma unroll
             for (int hi = 0; hi < 2; ++hi)
                 voff[cb][hi] = kv_off(4 * (tr_g >> 1) + tr_e + 8 * hi, 32 * cb + 16 * (tr_g & 1) + 4 * tr_q);
-        for (int qb = wave; qb * 32 < L; qb += kAttnWaves) {
+        for (int qb = CAUSAL ? snake_block(wave) : wave; qb * 32 < L; qb += kAttnWaves) {
             const int qi = min(qb * 32 + l32, L - 1);
+            const int n_chunks = CAUSAL ? qb + 1 : nc;  // masked: keys up to the block's last query
             const uint16_t* qrow = q + (int64_t)(t0 + qi) * ldq + h * kHeadDim + 8 * h2;
             bf16x8 qf[4];
 #pragma unroll
@@ -490,7 +513,7 @@ void k_attention_bf16(PlanArgs pa, const int32_t* __restrict__ order, const uint
             // per-lane LDS pointers of chunk 0, advanced by 32 rows per chunk
             const uint16_t* kp = ks_ + koff[0];
             const uint16_t* vp = vs_;
-            for (int c = 0; c < nc; ++c, kp += 32 * kHeadDim, vp += 32 * kHeadDim) {
+            for (int c = 0; c < n_chunks; ++c, kp += 32 * kHeadDim, vp += 32 * kHeadDim) {
                 floatx16 acc;
 #pragma unroll
                 for (int r = 0; r < 16; ++r) acc[r] = 0.f;
@@ -501,10 +524,13 @@ void k_attention_bf16(PlanArgs pa, const int32_t* __restrict__ order, const uint
                 __builtin_amdgcn_sched_barrier(0);  // all four reads in flight before the first MFMA waits
 #pragma unroll
                 for (int ks = 0; ks < 4; ++ks) acc = mfma32x32x16(kf[ks], qf[ks], acc);
-                if (32 * (c + 1) > L) {  // keys past the sequence take no part (wave-uniform branch)
+                // keys past the sequence (and, masked, keys after the query) take no part;
+                // the branch is wave-uniform
+                if (32 * (c + 1) > L || (CAUSAL && c == qb)) {
+                    const int kmax = CAUSAL && c == qb ? min(L - 1, qb * 32 + l32) : L - 1;
 #pragma unroll
                     for (int r = 0; r < 16; ++r)
-                        if (32 * c + 8 * (r / 4) + 4 * h2 + (r % 4) >= L) acc[r] = -INFINITY;
+                        if (32 * c + 8 * (r / 4) + 4 * h2 + (r % 4) > kmax) acc[r] = -INFINITY;
                 }
                 float cmax = acc[0];
 #pragma unroll
@@ -571,51 +597,54 @@ int persistent_grid(int64_t cap, int per_cu) {
 }  // namespace
 
 hipError_t launch_qkt(const PlanView& p, int dtype, const void* q, int ldq, const void* k, int ldk, float scale,
-                      void* scores, int64_t score_cap, hipStream_t s) {
+                      void* scores, int64_t score_cap, bool causal, hipStream_t s) {
     const PlanArgs pa = plan_args(p);
     const int grid = persistent_grid(p.qkt_cap, 8);
     if (dtype == 1)
         hipLaunchKernelGGL(k_qkt_bf16, dim3(grid), dim3(256), 0, s, pa, static_cast<const uint16_t*>(q), ldq,
-                           static_cast<const uint16_t*>(k), ldk, scale, static_cast<uint16_t*>(scores), score_cap);
+                           static_cast<const uint16_t*>(k), ldk, scale, static_cast<uint16_t*>(scores), score_cap,
+                           int(causal));
     else
         hipLaunchKernelGGL(k_qkt_f32, dim3(grid), dim3(256), 0, s, pa, static_cast<const float*>(q), ldq,
-                           static_cast<const float*>(k), ldk, scale, static_cast<float*>(scores), score_cap);
+                           static_cast<const float*>(k), ldk, scale, static_cast<float*>(scores), score_cap,
+                           int(causal));
     return hipGetLastError();
 }
 
 hipError_t launch_softmax(const PlanView& p, int dtype, const void* scores, void* probs, int64_t score_cap,
-                          hipStream_t s) {
+                          bool causal, hipStream_t s) {
     if (p.total_tokens == 0) return hipSuccess;
     const PlanArgs pa = plan_args(p);
     const int grid = (p.total_tokens + 3) / 4;
     if (dtype == 1)
         hipLaunchKernelGGL(k_softmax<true>, dim3(grid), dim3(256), 0, s, pa, static_cast<const uint16_t*>(scores),
-                           static_cast<uint16_t*>(probs), score_cap, p.total_tokens);
+                           static_cast<uint16_t*>(probs), score_cap, p.total_tokens, int(causal));
     else
         hipLaunchKernelGGL(k_softmax<false>, dim3(grid), dim3(256), 0, s, pa, static_cast<const float*>(scores),
-                           static_cast<float*>(probs), score_cap, p.total_tokens);
+                           static_cast<float*>(probs), score_cap, p.total_tokens, int(causal));
     return hipGetLastError();
 }
 
 hipError_t launch_attn_v(const PlanView& p, int dtype, const void* probs, int64_t score_cap, const void* v, int ldv,
-                         void* out, int ldo, hipStream_t s) {
+                         void* out, int ldo, bool causal, hipStream_t s) {
     const PlanArgs pa = plan_args(p);
     const int grid = persistent_grid(p.av_cap, 8);
     if (dtype == 1)
         hipLaunchKernelGGL(k_attn_v_bf16, dim3(grid), dim3(256), 0, s, pa, static_cast<const uint16_t*>(probs),
-                           score_cap, static_cast<const uint16_t*>(v), ldv, static_cast<uint16_t*>(out), ldo);
+                           score_cap, static_cast<const uint16_t*>(v), ldv, static_cast<uint16_t*>(out), ldo, int(causal));
     else
         hipLaunchKernelGGL(k_attn_v_f32, dim3(grid), dim3(256), 0, s, pa, static_cast<const float*>(probs),
-                           score_cap, static_cast<const float*>(v), ldv, static_cast<float*>(out), ldo);
+                           score_cap, static_cast<const float*>(v), ldv, static_cast<float*>(out), ldo, int(causal));
     return hipGetLastError();
 }
 
-hipError_t launch_fused_attention(const PlanView& p, int dtype, const void* q, int ldq, const void* k, int ldk,
-                                  const void* v, int ldv, float scale, void* out, int ldo, hipStream_t s) {
-    if (dtype != 1 || p.max_len > kAttnMaxLen) return hipErrorInvalidValue;
+namespace {
+template <bool CAUSAL>
+hipError_t launch_fused_variant(const PlanView& p, const void* q, int ldq, const void* k, int ldk, const void* v,
+                                int ldv, float scale, void* out, int ldo, hipStream_t s) {
     static bool attr_set = false;  // benign race: every thread sets the same value
     if (!attr_set) {
-        hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_attention_bf16),
+        hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_attention_bf16<CAUSAL>),
                                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)kAttnLds);
         if (e != hipSuccess) return e;
         attr_set = true;
@@ -623,10 +652,19 @@ hipError_t launch_fused_attention(const PlanView& p, int dtype, const void* q, i
     const PlanArgs pa = plan_args(p);
     const int64_t pairs = (int64_t)p.batch * p.heads;
     const int grid = static_cast<int>(std::min<int64_t>(pairs, device_cu_count()));
-    hipLaunchKernelGGL(k_attention_bf16, dim3(grid), dim3(kAttnThreads), kAttnLds, s, pa, p.order,
+    hipLaunchKernelGGL(k_attention_bf16<CAUSAL>, dim3(grid), dim3(kAttnThreads), kAttnLds, s, pa, p.order,
                        static_cast<const uint16_t*>(q), ldq, static_cast<const uint16_t*>(k), ldk,
                        static_cast<const uint16_t*>(v), ldv, scale, static_cast<uint16_t*>(out), ldo);
     return hipGetLastError();
+}
+}  // namespace
+
+hipError_t launch_fused_attention(const PlanView& p, int dtype, const void* q, int ldq, const void* k, int ldk,
+                                  const void* v, int ldv, float scale, void* out, int ldo, bool causal,
+                                  hipStream_t s) {
+    if (dtype != 1 || p.max_len > kAttnMaxLen) return hipErrorInvalidValue;
+    return causal ? launch_fused_variant<true>(p, q, ldq, k, ldk, v, ldv, scale, out, ldo, s)
+                  : launch_fused_variant<false>(p, q, ldq, k, ldk, v, ldv, scale, out, ldo, s);
 }
 
 }  // namespace rag

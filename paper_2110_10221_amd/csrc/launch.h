@@ -30,15 +30,16 @@ hipError_t launch_offsets(const PlanView& p, hipStream_t s);
 
 // Attention operators; dtype 0 = fp32, 1 = bf16.  Persistent grids sized from the
 // host-side capacities; item counts are read on the device.
+// `causal` selects masked attention (position i sees keys j <= i).
 hipError_t launch_qkt(const PlanView& p, int dtype, const void* q, int ldq, const void* k, int ldk,
-                      float scale, void* scores, int64_t score_cap, hipStream_t s);
+                      float scale, void* scores, int64_t score_cap, bool causal, hipStream_t s);
 hipError_t launch_softmax(const PlanView& p, int dtype, const void* scores, void* probs,
-                          int64_t score_cap, hipStream_t s);
+                          int64_t score_cap, bool causal, hipStream_t s);
 hipError_t launch_attn_v(const PlanView& p, int dtype, const void* probs, int64_t score_cap,
-                         const void* v, int ldv, void* out, int ldo, hipStream_t s);
+                         const void* v, int ldv, void* out, int ldo, bool causal, hipStream_t s);
 hipError_t launch_fused_attention(const PlanView& p, int dtype, const void* q, int ldq, const void* k,
                                   int ldk, const void* v, int ldv, float scale, void* out, int ldo,
-                                  hipStream_t s);
+                                  bool causal, hipStream_t s);
 
 hipError_t launch_linear(int dtype, const void* x, int ldx, const void* w, const void* bias,
                          const void* residual, int ldr, int act, void* y, int ldy, int T, int K, int N,
