@@ -33,15 +33,24 @@ METRIC = "ms/encoder layer + useful (unpadded) TFLOP/s, fraction of bf16 MFMA pe
 
 # stage index (events[k] .. events[k+1]) -> kernel symbol
 STAGES = ["qkv_proj", "qkt", "softmax", "attention", "out_proj", "layernorm1", "ff1", "ff2", "layernorm2"]
-STAGE_KERNEL = {
-    "qkv_proj": "k_gemm_bf16<0, true, false>",
-    "attention": "k_attention_bf16",
-    "out_proj": "k_gemm_bf16<0, true, true>",
-    "ff2": "k_gemm_bf16<0, true, true>",
-    "ff1": "k_gemm_bf16<1, true, false>",
-    "layernorm1": "k_layernorm<true, 2>",
-    "layernorm2": "k_layernorm<true, 2>",
-}
+
+
+def stage_kernels(T, d, dff):
+    """Kernel symbol of each timed stage of the bf16 layer with fused attention, following the
+    library's launch rules: 256-token GEMM tiles for wide plain outputs, 128 otherwise;
+    LayerNorm instantiated for the power of two >= d / 512 16-byte chunks per lane."""
+    bm_qkv = 256 if 3 * d >= 2048 and T >= 2048 else 128
+    chunks = -(-d // 8 // 64)  # 16-byte chunks per lane, rounded up to a power of two
+    ln = f"k_layernorm<true, {1 << max(0, (chunks - 1).bit_length())}>"
+    return {
+        "qkv_proj": f"k_gemm_bf16<{bm_qkv}, 0, true, false>",
+        "attention": "k_attention_bf16<false>",
+        "out_proj": "k_gemm_bf16<128, 0, true, true>",
+        "ff2": "k_gemm_bf16<128, 0, true, true>",
+        "ff1": "k_gemm_bf16<128, 1, true, false>",
+        "layernorm1": ln,
+        "layernorm2": ln,
+    }
 KERNEL_SOURCES = {
     "k_gemm_bf16": "paper_2110_10221_amd/csrc/gemm.hip",
     "k_attention_bf16": "paper_2110_10221_amd/csrc/attention.hip",
@@ -173,7 +182,7 @@ def _counter_per_dispatch(path, counter):
 
 
 def _short(name):
-    """Demangled kernel name -> 'k_name<args>' as used in STAGE_KERNEL."""
+    """Demangled kernel name -> 'k_name<args>' as returned by stage_kernels()."""
     base = name.replace("rag::(anonymous namespace)::", "").replace("void ", "", 1)
     return base.split("(")[0].strip()
 
@@ -340,7 +349,7 @@ def main():
     work = stage_work(T, d, H, dff, s2)
     # group stages by kernel symbol; the dominant kernel has the largest total time
     per_kernel = {}
-    for s, kname in STAGE_KERNEL.items():
+    for s, kname in stage_kernels(T, d, dff).items():
         fl, by = work[s]
         pk = per_kernel.setdefault(kname, {"ms": 0.0, "flops": 0.0, "bytes": 0.0, "launches": 0})
         pk["ms"] += stage_ms[s]

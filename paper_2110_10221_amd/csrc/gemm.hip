@@ -99,15 +99,19 @@ __device__ __forceinline__ bf16x8 lds_frag(const uint16_t* tile, int row, int ch
 }
 
 // Output tile of a linear workgroup id.  Workgroups are dealt to the 8 XCDs
-// round-robin, so the id is first remapped to give each XCD a contiguous range;
-// that range is walked in groups of kGroupM token tiles, token tile fastest, so
-// the tiles an XCD runs at once share both x rows and w rows in its L2.
-__device__ __forceinline__ void tile_coords(int bid, int nblocks, int tiles_m, int tiles_n, int& tm, int& tn) {
+// round-robin, so the id is first remapped to give each XCD a contiguous range.
+// That range is walked in groups of kGroupM token tiles, token tile fastest, so
+// the tiles an XCD runs at once share both x rows and w rows in its L2 -- except
+// for a narrow output with a long K (few feature tiles, x tiles of 1 MB and
+// more), where token-major order lets the workgroups that start together share
+// each x tile (measured faster there).
+__device__ __forceinline__ void tile_coords(int bid, int nblocks, int tiles_m, int tiles_n, int K, int& tm, int& tn) {
     const int per = nblocks / 8, rem = nblocks % 8;
     const int xcd = bid % 8, idx = bid / 8;
     const int t = xcd < rem ? xcd * (per + 1) + idx : rem * (per + 1) + (xcd - rem) * per + idx;
-    const int gsz = kGroupM * tiles_n, first = (t / gsz) * kGroupM;
-    const int gm = min(tiles_m - first, kGroupM);
+    const int group = (tiles_n < 8 && K > 2048) ? 1 : kGroupM;
+    const int gsz = group * tiles_n, first = (t / gsz) * group;
+    const int gm = min(tiles_m - first, group);
     tm = first + (t % gsz) % gm;
     tn = (t % gsz) / gm;
 }
@@ -131,7 +135,7 @@ void k_gemm_bf16(const uint16_t* __restrict__ x, int ldx, const uint16_t* __rest
     constexpr int kStages = C::kStages, kStageElems = C::kStageElems, kCopies = C::kCopies;
     extern __shared__ __attribute__((aligned(16))) uint16_t smem[];
     int tm, tn;
-    tile_coords(blockIdx.x, gridDim.x, tiles_m, tiles_n, tm, tn);
+    tile_coords(blockIdx.x, gridDim.x, tiles_m, tiles_n, K, tm, tn);
     const int m0 = tm * BM, n0 = tn * BN;
     const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
     const int wm = wave / 4, wn = wave % 4;
