@@ -13,6 +13,7 @@ from __future__ import annotations
 import ctypes
 import os
 import subprocess
+from typing import NamedTuple
 
 import numpy as np
 
@@ -58,6 +59,9 @@ def lib():
         l.oracle_encoder_layer.argtypes = [ctypes.c_int, i32, p, i32, i32, i32, f64, ctypes.c_int, ctypes.c_int, p, p,
                                            p]
         l.oracle_round_bf16.argtypes = [i64, p, p]
+        l.oracle_vgemm_offsets.restype = ctypes.c_int
+        l.oracle_vgemm_offsets.argtypes = [i32, p, i32, i32, p, p, p, p, p]
+        l.oracle_vgemm.argtypes = [ctypes.c_int, i32, p, p, p, p]
         _lib = l
     return _lib
 
@@ -190,3 +194,37 @@ def encoder_layer(dtype, lengths, x, weights: dict, d_model, heads, d_ff, eps=1e
     if rc != 0:
         raise MemoryError("oracle_encoder_layer: allocation failed")
     return out[:T]
+
+
+VGEMM_TILE_M, VGEMM_TILE_N = 128, 256
+
+
+class VgemmOffsets(NamedTuple):
+    a_off: np.ndarray
+    b_off: np.ndarray
+    c_off: np.ndarray
+    order: np.ndarray
+    tile_off: np.ndarray
+
+
+def vgemm_offsets(dims, tile_m=VGEMM_TILE_M, tile_n=VGEMM_TILE_N) -> VgemmOffsets:
+    """Packed-storage offsets, largest-first order and tile prefix of a vgemm batch;
+    dims is [B, 3] (m, n, k)."""
+    d = np.ascontiguousarray(np.asarray(dims, np.int32).reshape(-1, 3))
+    B = d.shape[0]
+    a, b, c, t = (np.zeros(B + 1, np.int64) for _ in range(4))
+    order = np.zeros(max(B, 1), np.int32)
+    rc = lib().oracle_vgemm_offsets(B, _ptr(d), tile_m, tile_n, _ptr(a), _ptr(b), _ptr(c), _ptr(order), _ptr(t))
+    if rc != 0:
+        raise ValueError("negative vgemm size")
+    return VgemmOffsets(a, b, c, order[:B], t)
+
+
+def vgemm(dtype, dims, a, b):
+    """C_b = A_b B_b^T for every problem of the packed batch (storage form in and out)."""
+    d = np.ascontiguousarray(np.asarray(dims, np.int32).reshape(-1, 3))
+    c_elems = int((d[:, 0].astype(np.int64) * d[:, 1]).sum())
+    c = np.zeros(max(c_elems, 1), _storage_dtype(dtype))
+    lib().oracle_vgemm(_DT[dtype], d.shape[0], _ptr(d), _ptr(np.ascontiguousarray(a)), _ptr(np.ascontiguousarray(b)),
+                       _ptr(c))
+    return c[:c_elems]

@@ -428,3 +428,72 @@ done:
     free(qkv); free(s); free(o); free(y1); free(h1); free(f); free(y2);
     return rc;
 }
+
+/* ------------------------------------------------------------------------ */
+/* Variable-sized batched GEMM (vgemm, Section 7.1)                           */
+/* ------------------------------------------------------------------------ */
+
+/*
+ * vgemm: a batch of B independent GEMMs with their own sizes (m_b, n_b, k_b),
+ * stored ragged: the problems' matrices are packed one after another, each
+ * row-major, and located through exclusive prefix sums of their sizes (the
+ * storage of a ragged dimension, Section 5.3 / Appendix B):
+ *   a_off[b] = sum_{b' < b} m_b' * k_b'    A_b is [m_b, k_b]
+ *   b_off[b] = sum_{b' < b} n_b' * k_b'    B_b is [n_b, k_b] (rows are the
+ *                                          output columns, k contiguous)
+ *   c_off[b] = sum_{b' < b} m_b' * n_b'    C_b is [m_b, n_b]
+ * Work is ordered largest first (Appendix D, load balancing): order[] sorts
+ * the problems by m*n*k descending, ties by lower index; tile_off[] is the
+ * exclusive prefix sum, in that order, of each problem's
+ * ceil(m/tile_m) * ceil(n/tile_n) output tiles.  dims holds (m, n, k) per
+ * problem.  Returns 0, or 1 if a size is negative.
+ */
+int oracle_vgemm_offsets(int32_t B, const int32_t* dims, int32_t tile_m, int32_t tile_n, int64_t* a_off,
+                         int64_t* b_off, int64_t* c_off, int32_t* order, int64_t* tile_off) {
+    for (int32_t b = 0; b < B; ++b)
+        if (dims[3 * b] < 0 || dims[3 * b + 1] < 0 || dims[3 * b + 2] < 0) return 1;
+    a_off[0] = b_off[0] = c_off[0] = 0;
+    for (int32_t b = 0; b < B; ++b) {
+        int64_t m = dims[3 * b], n = dims[3 * b + 1], k = dims[3 * b + 2];
+        a_off[b + 1] = a_off[b] + m * k;
+        b_off[b + 1] = b_off[b] + n * k;
+        c_off[b + 1] = c_off[b] + m * n;
+    }
+    for (int32_t b = 0; b < B; ++b) order[b] = b;
+    for (int32_t i = 1; i < B; ++i) {  /* stable insertion sort, work descending */
+        int32_t cur = order[i];
+        int64_t wc = (int64_t)dims[3 * cur] * dims[3 * cur + 1] * dims[3 * cur + 2];
+        int32_t p = i - 1;
+        while (p >= 0 && (int64_t)dims[3 * order[p]] * dims[3 * order[p] + 1] * dims[3 * order[p] + 2] < wc) {
+            order[p + 1] = order[p];
+            --p;
+        }
+        order[p + 1] = cur;
+    }
+    tile_off[0] = 0;
+    for (int32_t i = 0; i < B; ++i) {
+        int32_t b = order[i];
+        tile_off[i + 1] = tile_off[i] + ceil_div(dims[3 * b], tile_m) * ceil_div(dims[3 * b + 1], tile_n);
+    }
+    return 0;
+}
+
+/*
+ * vgemm product: for every problem b, C_b[i][j] = rd(sum_k A_b[i][k] * B_b[j][k]),
+ * i < m_b, j < n_b, on the packed storage above.
+ */
+void oracle_vgemm(int dtype, int32_t B, const int32_t* dims, const void* a, const void* bm, void* c) {
+    int64_t ao = 0, bo = 0, co = 0;
+    for (int32_t p = 0; p < B; ++p) {
+        int64_t m = dims[3 * p], n = dims[3 * p + 1], k = dims[3 * p + 2];
+        for (int64_t i = 0; i < m; ++i)
+            for (int64_t j = 0; j < n; ++j) {
+                double acc = 0.0;
+                for (int64_t t = 0; t < k; ++t) acc += load(a, dtype, ao + i * k + t) * load(bm, dtype, bo + j * k + t);
+                store(c, dtype, co + i * n + j, acc);
+            }
+        ao += m * k;
+        bo += n * k;
+        co += m * n;
+    }
+}
