@@ -249,6 +249,70 @@ def masked_measurement(rag, plan, wl, x, wstruct, ws, y, flags, iters=20):
             "note": "fused causal attention and the masked layer (plan included once, not per call)"}
 
 
+def vgemm_measurement(rag, batch=128, iters=20):
+    """Variable-sized batched GEMM (the paper's matrix-multiplication experiment):
+    `batch` problems with m, n, k uniform over the multiples of 128 in [512, 1408],
+    packed operands, against two library stand-ins on the same sizes: a fully
+    padded batched GEMM (every problem padded to the largest m, n, k; torch.bmm)
+    and one library GEMM per problem (torch.matmul in a loop).  Useful FLOPs are
+    2 * sum m n k for all three."""
+    import torch
+
+    from workloads import draw_vgemm_dims
+
+    dims = draw_vgemm_dims(batch, np.random.default_rng(batch))
+    d64 = dims.astype(np.int64)
+    a_n, b_n, c_n = (int(v) for v in ((d64[:, 0] * d64[:, 2]).sum(), (d64[:, 1] * d64[:, 2]).sum(),
+                                       (d64[:, 0] * d64[:, 1]).sum()))
+    g = torch.Generator(device="cuda").manual_seed(2)
+    a = torch.randn(a_n, device="cuda", generator=g).bfloat16()
+    b = torch.randn(b_n, device="cuda", generator=g).bfloat16()
+    c = torch.empty(c_n, device="cuda", dtype=torch.bfloat16)
+    plan = rag.VgemmPlan(torch.from_numpy(dims).cuda(), host_dims=dims)
+    rag.vgemm_offsets(plan)
+
+    def timed(fn):
+        for _ in range(3):
+            fn()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(iters):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / iters
+
+    ms = timed(lambda: rag.ragged_vgemm(plan, a, b, c))
+    assert not plan.data_errors(), plan.data_errors()
+    ms_plan = timed(lambda: rag.vgemm_offsets(plan))
+    useful = 2.0 * float((d64[:, 0] * d64[:, 1] * d64[:, 2]).sum())
+    M, N, K = (int(v) for v in dims.max(axis=0))
+    ap = torch.randn(batch, M, K, device="cuda", generator=g).bfloat16()
+    bp = torch.randn(batch, K, N, device="cuda", generator=g).bfloat16()   # contiguous [K, N] right operands
+    cp = torch.empty(batch, M, N, device="cuda", dtype=torch.bfloat16)
+    ms_pad = timed(lambda: torch.bmm(ap, bp, out=cp))
+    del ap, bp, cp
+    offs = np.concatenate([[0], np.cumsum(d64[:, 0] * d64[:, 2])]), np.concatenate([[0], np.cumsum(d64[:, 1] * d64[:, 2])])
+    coff = np.concatenate([[0], np.cumsum(d64[:, 0] * d64[:, 1])])
+    views = [(a[offs[0][p]:offs[0][p + 1]].view(m, k), b[offs[1][p]:offs[1][p + 1]].view(n, k).t(),
+              c[coff[p]:coff[p + 1]].view(m, n)) for p, (m, n, k) in enumerate(d64.tolist())]
+
+    def per_problem():
+        for x, wt, y in views:
+            torch.matmul(x, wt, out=y)
+
+    ms_loop = timed(per_problem)
+    tf = useful / (ms * 1e-3) / 1e12
+    return {"workload": f"vgemm, batch {batch}, m n k uniform over multiples of 128 in [512, 1408] (seed {batch})",
+            "ms": round(ms, 4), "useful_tflops": round(tf, 1), "frac_of_bf16_peak": round(tf / PEAK_BF16_TFLOPS, 4),
+            "kernel": "k_vgemm_bf16", "tiles": plan.n_tiles(), "plan_ms": round(ms_plan, 4),
+            "padded_bmm_ms": round(ms_pad, 4), "speedup_vs_padded_bmm": round(ms_pad / ms, 3),
+            "per_problem_matmul_ms": round(ms_loop, 4), "speedup_vs_per_problem_matmul": round(ms_loop / ms, 3),
+            "useful_fraction_of_padded": round(useful / (2.0 * batch * M * N * K), 4),
+            "note": "library stand-ins run hipBLASLt through torch on the same sizes (padded: every problem "
+                    "at the batch's largest m, n, k)"}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -259,6 +323,7 @@ def main():
     ap.add_argument("--flags", type=int, default=0, help="encoder_layer flags (1 = unfused attention)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-masked", action="store_true", help="skip the masked (causal) attention measurement")
+    ap.add_argument("--no-vgemm", action="store_true", help="skip the variable-sized batched GEMM measurement")
     ap.add_argument("--cpu-target-flops", type=float, default=2.0e10)
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of MIB MiB five times (counter calibration) and exit")
@@ -405,6 +470,8 @@ def main():
     }
     if not args.no_masked:
         out["masked"] = masked_measurement(rag, plan, wl, x, wstruct, ws, y, args.flags)
+    if not args.no_vgemm:
+        out["vgemm"] = vgemm_measurement(rag)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(wl, args.cpu_target_flops)
     else:

@@ -257,6 +257,99 @@ rag_status packed_layernorm(const void* x, int32_t ldx, const void* gamma, const
                             float eps, void* y, int32_t ldy, int32_t T, int32_t d, int32_t dtype,
                             void* stream);
 
+/*
+ * Variable-sized batched GEMM (vgemm; Section 7.1, the matrix-multiplication
+ * experiments): a batch of B independent products with their own sizes,
+ *   C_b[i][j] = sum_{l < k_b} A_b[i][l] * B_b[j][l],   i < m_b, j < n_b,
+ * A_b [m_b, k_b], B_b [n_b, k_b] (both with the reduction dimension contiguous)
+ * and C_b [m_b, n_b], all row-major.  The three operands of the whole batch are
+ * stored packed, each problem right after the previous one with no padding:
+ * A_b starts at element a_off[b] of `a`, B_b at b_off[b] of `b`, C_b at c_off[b]
+ * of `c`.  The work is split into RAG_VGEMM_TILE_M x RAG_VGEMM_TILE_N tiles of
+ * the outputs; tiles at a problem's edge are predicated, never padded in memory.
+ */
+#define RAG_VGEMM_TILE_M 128
+#define RAG_VGEMM_TILE_N 256
+/* Largest batch a vgemm plan accepts, and largest m, n or k of one problem. */
+#define RAG_VGEMM_MAX_BATCH 4096
+#define RAG_VGEMM_MAX_DIM 65536
+/* Largest tile_cap a vgemm plan accepts. */
+#define RAG_VGEMM_MAX_TILES (1 << 30)
+
+/* Bits of a vgemm plan's status[0]. */
+enum {
+    RAG_VGEMM_NEG_SIZE = 1,     /* some m, n or k < 0                                */
+    RAG_VGEMM_LARGE_SIZE = 2,   /* some m, n or k > RAG_VGEMM_MAX_DIM                */
+    RAG_VGEMM_TILE_CAP = 4,     /* more output tiles than tile_cap                   */
+    RAG_VGEMM_OPERAND_CAP = 8,  /* (set by ragged_vgemm) a, b or c smaller than the
+                                   packed batch (a_off[B], b_off[B], c_off[B])       */
+    RAG_VGEMM_BF16_SHAPE = 16   /* (set by ragged_vgemm with RAG_BF16) some k % 64 or
+                                   n % 8 is not 0                                    */
+};
+
+/*
+ * The vgemm prelude's auxiliary arrays (the same role as rag_plan: they depend
+ * only on the sizes, so one plan serves every call on a batch of that shape).
+ * The caller fills the host fields and allocates every device array;
+ * vgemm_offsets() fills the arrays.
+ *   a_off, b_off, c_off [B+1]  exclusive prefix sums of m_b k_b, n_b k_b, m_b n_b
+ *   order[B]        problems by m_b n_b k_b (multiply-adds), largest first,
+ *                   ties by lower index (thread remapping, Section 4 and
+ *                   Appendix A.1: the largest work is scheduled first)
+ *   tile_off[B+1]   exclusive prefix sum, in `order` order, of the tile counts
+ *                   ceil(m_b / RAG_VGEMM_TILE_M) * ceil(n_b / RAG_VGEMM_TILE_N)
+ *   tile_items[4*n] (problem, tile row, tile column, 0) for every output tile:
+ *                   problems in `order`, tile rows fastest inside a problem;
+ *                   n = tile_off[B]
+ *   status[3]       {data-error bits, n, 1 if some problem breaks the bf16
+ *                   shape rule of ragged_vgemm (k_b % 64 == 0, n_b % 8 == 0)}
+ */
+typedef struct rag_vgemm_plan {
+    int32_t batch;          /* (host) B, 1 <= B <= RAG_VGEMM_MAX_BATCH           */
+    int64_t tile_cap;       /* (host) capacity of tile_items, in tiles,
+                               0 <= tile_cap <= RAG_VGEMM_MAX_TILES              */
+    const int32_t* dims;    /* [3*B] (m_b, n_b, k_b)                             */
+    int64_t* a_off;         /* [B+1]                                            */
+    int64_t* b_off;         /* [B+1]                                            */
+    int64_t* c_off;         /* [B+1]                                            */
+    int32_t* order;         /* [B]                                              */
+    int64_t* tile_off;      /* [B+1]                                            */
+    int32_t* tile_items;    /* [4*tile_cap], 16-byte aligned                    */
+    int32_t* status;        /* [3]                                              */
+} rag_vgemm_plan;
+
+/*
+ * (host only)  A tile_cap that always suffices when every m_b <= max_m and
+ * n_b <= max_n: batch * ceil(max_m / 128) * ceil(max_n / 256).  Launches
+ * nothing.  ragged_vgemm launches one workgroup per tile of tile_cap, so a
+ * capacity far above the real tile count costs idle workgroups.
+ */
+rag_status vgemm_plan_capacity(int32_t batch, int32_t max_m, int32_t max_n, int64_t* tile_cap /* (host) out */);
+
+/*
+ * Build the vgemm plan's device arrays from plan->dims.  The status word is
+ * rewritten from scratch.  Host errors: RAG_ERR_ARG for null or misaligned
+ * arrays and out-of-range host fields, RAG_ERR_CAPACITY if tile_cap exceeds
+ * RAG_VGEMM_MAX_TILES.
+ * Data errors (negative or too large sizes, too many tiles) go to status[0]
+ * and make ragged_vgemm return without writing.
+ */
+rag_status vgemm_offsets(rag_vgemm_plan* plan, void* stream);
+
+/*
+ * The vgemm itself over a plan built by vgemm_offsets(): every tile of every
+ * problem, largest problems first.  a, b and c hold a_cap, b_cap and c_cap
+ * elements; if the packed batch does not fit, nothing is written and
+ * RAG_VGEMM_OPERAND_CAP is set (like every data-error bit it stays set until
+ * vgemm_offsets() rebuilds the plan).  dtype RAG_BF16 (fp32 accumulation, products
+ * rounded to nearest even when stored) needs every k_b % 64 == 0 and every
+ * n_b % 8 == 0, else nothing is written and RAG_VGEMM_BF16_SHAPE is set; a,
+ * b, c must then be 16-byte aligned.  dtype RAG_F32 takes any sizes.  A problem
+ * with k_b == 0 gets C_b = 0.  c must not overlap a or b.
+ */
+rag_status ragged_vgemm(const rag_vgemm_plan* plan, const void* a, int64_t a_cap, const void* b,
+                        int64_t b_cap, void* c, int64_t c_cap, int32_t dtype, void* stream);
+
 /* encoder_layer flags */
 enum {
     RAG_LAYER_UNFUSED_ATTENTION = 1, /* run ragged_qkt/softmax/attn_v with a

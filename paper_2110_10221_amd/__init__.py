@@ -30,6 +30,10 @@ RAG_LAYER_CAUSAL = 2
 RAG_LAYER_EVENTS = 10
 DATA_BITS = {1: "negative length", 2: "length > max_len", 4: "sum of lengths != total_tokens",
              8: "qkt_cap exceeded", 16: "av_cap exceeded", 32: "score buffer too small"}
+RAG_VGEMM_TILE_M, RAG_VGEMM_TILE_N = 128, 256
+RAG_VGEMM_MAX_BATCH, RAG_VGEMM_MAX_DIM, RAG_VGEMM_MAX_TILES = 4096, 65536, 1 << 30
+VGEMM_DATA_BITS = {1: "negative size", 2: "size > RAG_VGEMM_MAX_DIM", 4: "tile_cap exceeded",
+                   8: "operand buffer too small", 16: "bf16 needs k % 64 == 0 and n % 8 == 0"}
 
 if not os.path.exists(LIB_PATH):
     raise ImportError(f"{LIB_PATH} is missing: build the HIP library first "
@@ -46,6 +50,11 @@ class RagPlan(ctypes.Structure):
                 ("lengths", _p), ("tok_off", _p), ("att_off", _p), ("order", _p), ("tok_seq", _p),
                 ("qkt_item_off", _p), ("av_item_off", _p), ("qkt_items", _p), ("av_items", _p),
                 ("status", _p)]
+
+
+class RagVgemmPlan(ctypes.Structure):
+    _fields_ = [("batch", _i32), ("tile_cap", _i64), ("dims", _p), ("a_off", _p), ("b_off", _p), ("c_off", _p),
+                ("order", _p), ("tile_off", _p), ("tile_items", _p), ("status", _p)]
 
 
 class RagLayerWeights(ctypes.Structure):
@@ -77,6 +86,9 @@ _c_attn_v_causal = _sig("ragged_attn_v_causal", list(_c_attn_v.argtypes))
 _c_attention_causal = _sig("ragged_attention_causal", list(_c_attention.argtypes))
 _c_linear = _sig("packed_linear", [_p, _i32, _p, _p, _p, _i32, _i32, _p, _i32, _i32, _i32, _i32, _i32, _p])
 _c_layernorm = _sig("packed_layernorm", [_p, _i32, _p, _p, _f32, _p, _i32, _i32, _i32, _i32, _p])
+_c_vgemm_capacity = _sig("vgemm_plan_capacity", [_i32, _i32, _i32, ctypes.POINTER(_i64)])
+_c_vgemm_offsets = _sig("vgemm_offsets", [ctypes.POINTER(RagVgemmPlan), _p])
+_c_vgemm = _sig("ragged_vgemm", [ctypes.POINTER(RagVgemmPlan), _p, _i64, _p, _i64, _p, _i64, _i32, _p])
 _c_ws = _sig("encoder_layer_workspace", [_i32, _i32, _i32, _i32, _i32, _i32, _i32, ctypes.POINTER(ctypes.c_size_t)])
 _c_layer = _sig("encoder_layer", [ctypes.POINTER(RagPlan), _p, _p, _i32, _i32, _i32, _i32, _f32, _i32, _i32,
                                   ctypes.POINTER(RagLayerWeights), _p, ctypes.c_size_t, _i32, _p, _p])
@@ -260,3 +272,71 @@ def encoder_layer(plan: Plan, x, y, weights, d_ff, workspace, heads=None, head_d
                                      ctypes.byref(w), _ptr(workspace), workspace.numel() * workspace.element_size(),
                                      _dtype_code(x), _stream(stream),
                                      None if events is None else ctypes.cast(events, ctypes.c_void_p)))
+
+
+def vgemm_plan_capacity(batch, max_m, max_n):
+    n = _i64()
+    _check("vgemm_plan_capacity", _c_vgemm_capacity(batch, max_m, max_n, ctypes.byref(n)))
+    return n.value
+
+
+class VgemmPlan:
+    """Device arrays of a vgemm batch's prelude, allocated with torch.
+
+    `dims` is an int32 device tensor [B, 3] of (m, n, k).  `tile_cap` defaults to
+    the exact tile count when `host_dims` (the same sizes on the host) is given,
+    else to the bound from `max_m` / `max_n`."""
+
+    def __init__(self, dims: torch.Tensor, tile_cap: int | None = None, host_dims=None, max_m=None, max_n=None):
+        if dims.dtype != torch.int32 or not dims.is_cuda or dims.dim() != 2 or dims.shape[1] != 3:
+            raise ValueError("dims must be a [B, 3] int32 device tensor")
+        if not dims.is_contiguous():
+            raise ValueError("dims must be contiguous")
+        dev = dims.device
+        B = dims.shape[0]
+        if tile_cap is None:
+            if host_dims is not None:
+                tile_cap = sum(-(-max(int(m), 0) // RAG_VGEMM_TILE_M) * -(-max(int(n), 0) // RAG_VGEMM_TILE_N)
+                               for m, n, _ in host_dims)
+            elif max_m is not None and max_n is not None:
+                tile_cap = vgemm_plan_capacity(B, max_m, max_n)
+            else:
+                raise ValueError("give tile_cap, host_dims or max_m and max_n")
+        i64 = dict(dtype=torch.int64, device=dev)
+        self.dims = dims
+        self.a_off, self.b_off, self.c_off = (torch.empty(B + 1, **i64) for _ in range(3))
+        self.order = torch.empty(B, dtype=torch.int32, device=dev)
+        self.tile_off = torch.empty(B + 1, **i64)
+        self.tile_items = torch.empty(max(4 * tile_cap, 4), dtype=torch.int32, device=dev)
+        self.status = torch.zeros(3, dtype=torch.int32, device=dev)
+        self.batch, self.tile_cap = B, tile_cap
+        self.c = RagVgemmPlan(B, tile_cap, dims.data_ptr(), self.a_off.data_ptr(), self.b_off.data_ptr(),
+                              self.c_off.data_ptr(), self.order.data_ptr(), self.tile_off.data_ptr(),
+                              self.tile_items.data_ptr(), self.status.data_ptr())
+
+    def ref(self):
+        return ctypes.byref(self.c)
+
+    def data_errors(self):
+        """Decode status[0] (synchronises)."""
+        f = int(self.status[0].item())
+        return [msg for bit, msg in VGEMM_DATA_BITS.items() if f & bit]
+
+    def n_tiles(self):
+        return int(self.status[1].item())
+
+
+def vgemm_offsets(plan: VgemmPlan, stream=None):
+    _check("vgemm_offsets", _c_vgemm_offsets(plan.ref(), _stream(stream)))
+
+
+def ragged_vgemm(plan: VgemmPlan, a, b, c, stream=None):
+    """C_b = A_b B_b^T for every problem of the packed batch: a, b, c are 1-D
+    tensors of one dtype holding the packed operands."""
+    if not (a.dtype == b.dtype == c.dtype):
+        raise TypeError("a, b and c must share one dtype")
+    for t in (a, b, c):
+        if not t.is_contiguous():
+            raise ValueError("a, b and c must be contiguous")
+    _check("ragged_vgemm", _c_vgemm(plan.ref(), _ptr(a), a.numel(), _ptr(b), b.numel(), _ptr(c), c.numel(),
+                                    _dtype_code(a), _stream(stream)))

@@ -474,4 +474,65 @@ rag_status encoder_layer(const rag_plan* plan, const void* x, void* y, int32_t d
     return finish(e, s, plan->status, fn);
 }
 
+namespace {
+
+rag_status view_vgemm_plan(const rag_vgemm_plan* p, rag::VgemmView& v, const char* fn) {
+    if (!p) return fail(RAG_ERR_ARG, "%s: plan is NULL", fn);
+    if (p->batch < 1 || p->batch > RAG_VGEMM_MAX_BATCH)
+        return fail(RAG_ERR_ARG, "%s: batch %d outside [1, %d]", fn, p->batch, RAG_VGEMM_MAX_BATCH);
+    if (p->tile_cap < 0) return fail(RAG_ERR_ARG, "%s: negative tile_cap", fn);
+    if (p->tile_cap > RAG_VGEMM_MAX_TILES)
+        return fail(RAG_ERR_CAPACITY, "%s: tile_cap %lld exceeds %d", fn, (long long)p->tile_cap, RAG_VGEMM_MAX_TILES);
+    if (!p->dims || !p->a_off || !p->b_off || !p->c_off || !p->order || !p->tile_off || !p->status)
+        return fail(RAG_ERR_ARG, "%s: a plan array is NULL", fn);
+    if (p->tile_cap > 0 && (!p->tile_items || !aligned(p->tile_items, 16)))
+        return fail(RAG_ERR_ARG, "%s: tile_items must be non-NULL and 16-byte aligned", fn);
+    if (!aligned(p->dims, 4) || !aligned(p->a_off, 8) || !aligned(p->b_off, 8) || !aligned(p->c_off, 8) ||
+        !aligned(p->order, 4) || !aligned(p->tile_off, 8) || !aligned(p->status, 4))
+        return fail(RAG_ERR_ARG, "%s: misaligned plan array", fn);
+    v = rag::VgemmView{p->batch, p->tile_cap, p->dims, p->a_off, p->b_off, p->c_off, p->order,
+                       p->tile_off, p->tile_items, p->status};
+    return RAG_OK;
+}
+
+}  // namespace
+
+rag_status vgemm_plan_capacity(int32_t batch, int32_t max_m, int32_t max_n, int64_t* tile_cap) {
+    const char* fn = "vgemm_plan_capacity";
+    if (!tile_cap) return fail(RAG_ERR_ARG, "%s: output pointer is NULL", fn);
+    if (batch < 1 || batch > RAG_VGEMM_MAX_BATCH || max_m < 0 || max_n < 0 || max_m > RAG_VGEMM_MAX_DIM ||
+        max_n > RAG_VGEMM_MAX_DIM)
+        return fail(RAG_ERR_ARG, "%s: sizes out of range", fn);
+    *tile_cap = (int64_t)batch * ((max_m + RAG_VGEMM_TILE_M - 1) / RAG_VGEMM_TILE_M) *
+                ((max_n + RAG_VGEMM_TILE_N - 1) / RAG_VGEMM_TILE_N);
+    return RAG_OK;
+}
+
+rag_status vgemm_offsets(rag_vgemm_plan* plan, void* stream) {
+    const char* fn = "vgemm_offsets";
+    rag::VgemmView v;
+    rag_status st = view_vgemm_plan(plan, v, fn);
+    if (st) return st;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    return finish(rag::launch_vgemm_offsets(v, s), s, plan->status, fn);
+}
+
+rag_status ragged_vgemm(const rag_vgemm_plan* plan, const void* a, int64_t a_cap, const void* b, int64_t b_cap,
+                        void* c, int64_t c_cap, int32_t dtype, void* stream) {
+    const char* fn = "ragged_vgemm";
+    rag::VgemmView v;
+    rag_status st;
+    if ((st = view_vgemm_plan(plan, v, fn)) || (st = check_dtype(dtype, fn))) return st;
+    if (a_cap < 0 || b_cap < 0 || c_cap < 0) return fail(RAG_ERR_ARG, "%s: negative operand capacity", fn);
+    if ((a_cap && !a) || (b_cap && !b) || (c_cap && !c)) return fail(RAG_ERR_ARG, "%s: a, b or c is NULL", fn);
+    const size_t align = dtype == RAG_BF16 ? 16 : 4;
+    if (!aligned(a, align) || !aligned(b, align) || !aligned(c, align))
+        return fail(RAG_ERR_SHAPE, "%s: a, b and c must be %zu-byte aligned", fn, align);
+    const size_t es = elem_size(dtype);
+    if (ranges_overlap(c, c_cap * es, a, a_cap * es) || ranges_overlap(c, c_cap * es, b, b_cap * es))
+        return fail(RAG_ERR_ARG, "%s: c overlaps a or b", fn);
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    return finish(rag::launch_vgemm(v, dtype, a, a_cap, b, b_cap, c, c_cap, s), s, plan->status, fn);
+}
+
 }  // extern "C"

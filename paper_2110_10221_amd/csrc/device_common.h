@@ -20,6 +20,12 @@ constexpr int kHeadDim = 64;  // head dimension the attention kernels are built 
 constexpr int kDataNegLength = 1, kDataLongLength = 2, kDataTokenCount = 4, kDataQktCap = 8,
               kDataAvCap = 16, kDataScoreCap = 32;
 
+// Variable-sized batched GEMM: output tile, size limits and status-word bits
+// (mirror the public constants).
+constexpr int kVgemmTileM = 128, kVgemmTileN = 256, kVgemmMaxBatch = 4096, kVgemmMaxDim = 65536;
+constexpr int kVgemmNegSize = 1, kVgemmLargeSize = 2, kVgemmTileCap = 4, kVgemmOperandCap = 8,
+              kVgemmBf16Shape = 16;
+
 __device__ __forceinline__ float bf16_to_f32(uint16_t b) {
     return __uint_as_float(static_cast<uint32_t>(b) << 16);
 }

@@ -126,17 +126,16 @@ __device__ __forceinline__ void wait_copies(int n) {
     else asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
 }
 
+// One BM x BN output tile at (m0, n0) of y = act(x w^T + bias) + residual, w being
+// [N, K] with K contiguous; smem holds Cfg<BM>::kLdsBytes.  Called by the workgroup
+// as a whole (it synchronises on LDS).
 template <int BM, int ACT, bool HAS_BIAS, bool HAS_RES>
-__global__ __launch_bounds__(Cfg<BM>::kThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
-void k_gemm_bf16(const uint16_t* __restrict__ x, int ldx, const uint16_t* __restrict__ w,
-                 const uint16_t* __restrict__ bias, const uint16_t* residual, int ldr, uint16_t* y, int ldy,
-                 int T, int K, int N, int tiles_m, int tiles_n) {
+__device__ __forceinline__ void gemm_tile_bf16(const uint16_t* __restrict__ x, int ldx, const uint16_t* __restrict__ w,
+                                               const uint16_t* __restrict__ bias, const uint16_t* residual, int ldr,
+                                               uint16_t* y, int ldy, int T, int K, int N, int m0, int n0,
+                                               uint16_t* smem) {
     using C = Cfg<BM>;
     constexpr int kStages = C::kStages, kStageElems = C::kStageElems, kCopies = C::kCopies;
-    extern __shared__ __attribute__((aligned(16))) uint16_t smem[];
-    int tm, tn;
-    tile_coords(blockIdx.x, gridDim.x, tiles_m, tiles_n, K, tm, tn);
-    const int m0 = tm * BM, n0 = tn * BN;
     const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
     const int wm = wave / 4, wn = wave % 4;
     const int l32 = lane % 32, h2 = lane / 32;
@@ -292,13 +291,23 @@ void k_gemm_bf16(const uint16_t* __restrict__ x, int ldx, const uint16_t* __rest
     }
 }
 
+template <int BM, int ACT, bool HAS_BIAS, bool HAS_RES>
+__global__ __launch_bounds__(Cfg<BM>::kThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
+void k_gemm_bf16(const uint16_t* __restrict__ x, int ldx, const uint16_t* __restrict__ w,
+                 const uint16_t* __restrict__ bias, const uint16_t* residual, int ldr, uint16_t* y, int ldy,
+                 int T, int K, int N, int tiles_m, int tiles_n) {
+    extern __shared__ __attribute__((aligned(16))) uint16_t smem[];
+    int tm, tn;
+    tile_coords(blockIdx.x, gridDim.x, tiles_m, tiles_n, K, tm, tn);
+    gemm_tile_bf16<BM, ACT, HAS_BIAS, HAS_RES>(x, ldx, w, bias, residual, ldr, y, ldy, T, K, N, tm * BM, tn * BN, smem);
+}
+
 // fp32: 64x64 tiles, K step 16, 4x4 outputs per thread, plain FMA.
 template <int ACT>
-__global__ __launch_bounds__(256) void k_gemm_f32(const float* __restrict__ x, int ldx, const float* __restrict__ w,
-                                                   const float* __restrict__ bias, const float* residual, int ldr,
-                                                   float* y, int ldy, int T, int K, int N) {
+__device__ __forceinline__ void gemm_tile_f32(const float* __restrict__ x, int ldx, const float* __restrict__ w,
+                                              const float* __restrict__ bias, const float* residual, int ldr,
+                                              float* y, int ldy, int T, int K, int N, int m0, int n0) {
     __shared__ float xs[16][64 + 1], ws[16][64 + 1];
-    const int m0 = blockIdx.x * 64, n0 = blockIdx.y * 64;
     const int tx = threadIdx.x % 16, ty = threadIdx.x / 16;
     float acc[4][4] = {};
     for (int k0 = 0; k0 < K; k0 += 16) {
@@ -337,6 +346,127 @@ __global__ __launch_bounds__(256) void k_gemm_f32(const float* __restrict__ x, i
             if (residual) o += residual[(int64_t)m * ldr + n];
             y[(int64_t)m * ldy + n] = o;
         }
+    }
+}
+
+template <int ACT>
+__global__ __launch_bounds__(256) void k_gemm_f32(const float* __restrict__ x, int ldx, const float* __restrict__ w,
+                                                   const float* __restrict__ bias, const float* residual, int ldr,
+                                                   float* y, int ldy, int T, int K, int N) {
+    gemm_tile_f32<ACT>(x, ldx, w, bias, residual, ldr, y, ldy, T, K, N, blockIdx.x * 64, blockIdx.y * 64);
+}
+
+// ---------------------------------------------------------------------------
+// Variable-sized batched GEMM: one workgroup per entry of the plan's tile list
+// (problems largest first).  The workgroup -> entry map deals the list to the
+// 8 XCDs in chunks of kVgemmChunk consecutive entries (workgroups go to the
+// XCDs round-robin), so the tiles an XCD runs together mostly come from one
+// problem and share its operand panels in that XCD's L2, while every XCD still
+// gets a share of the large problems first.
+// ---------------------------------------------------------------------------
+constexpr int kVgemmChunk = 16;
+constexpr int kVgemmGridQuantum = 8 * kVgemmChunk;  // the grid is a multiple of this
+
+struct VgemmArgs {
+    const int32_t* dims;
+    const int64_t* a_off;
+    const int64_t* b_off;
+    const int64_t* c_off;
+    const int4* items;
+    int32_t* status;
+    int batch;
+    int64_t a_cap, b_cap, c_cap;
+};
+
+// The status word may be written in these kernels (atomicOr), so the compiler
+// cannot keep the plan reads in scalar registers by itself; these are
+// workgroup-uniform and are made so explicitly (otherwise every buffer
+// descriptor built from them becomes a per-lane loop).
+__device__ __forceinline__ int uni(int v) { return __builtin_amdgcn_readfirstlane(v); }
+__device__ __forceinline__ int64_t uni64(int64_t v) {
+    const uint32_t lo = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(v));
+    const uint32_t hi = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(static_cast<uint64_t>(v) >> 32));
+    return static_cast<int64_t>((static_cast<uint64_t>(hi) << 32) | lo);
+}
+
+// The tile one workgroup computes: problem p, output rows [m0, m0 + 128) and
+// columns [n0, n0 + 256) of C_p = A_p B_p^T.
+struct VgemmTile {
+    int m, n, k, m0, n0;
+    int64_t a_off, b_off, c_off;
+};
+
+__device__ __forceinline__ VgemmTile vgemm_tile(const VgemmArgs& va, int e) {
+    const int4 it = va.items[e];
+    const int p = uni(it.x);
+    VgemmTile t;
+    t.m = uni(va.dims[3 * p]);
+    t.n = uni(va.dims[3 * p + 1]);
+    t.k = uni(va.dims[3 * p + 2]);
+    t.m0 = uni(it.y) * kVgemmTileM;
+    t.n0 = uni(it.z) * kVgemmTileN;
+    t.a_off = uni64(va.a_off[p]);
+    t.b_off = uni64(va.b_off[p]);
+    t.c_off = uni64(va.c_off[p]);
+    return t;
+}
+
+__device__ __forceinline__ int vgemm_entry(int bid) {
+    const int xcd = bid % 8, idx = bid / 8;
+    return ((idx / kVgemmChunk) * 8 + xcd) * kVgemmChunk + idx % kVgemmChunk;
+}
+
+// False if the plan reports a data error or this call cannot run on it; one
+// thread then records why and every workgroup returns.
+__device__ __forceinline__ bool vgemm_ok(const VgemmArgs& va, bool bf16) {
+    if (va.status[0] != 0) return false;
+    int bad = 0;
+    if (va.a_off[va.batch] > va.a_cap || va.b_off[va.batch] > va.b_cap || va.c_off[va.batch] > va.c_cap)
+        bad |= kVgemmOperandCap;
+    if (bf16 && va.status[2] != 0) bad |= kVgemmBf16Shape;
+    if (bad) {
+        if (blockIdx.x == 0 && threadIdx.x == 0) atomicOr(va.status, bad);
+        return false;
+    }
+    return true;
+}
+
+// C = 0 over the rows [m0, m) x columns [n0, n) of a tile (problems with k = 0).
+template <typename E>
+__device__ __forceinline__ void vgemm_zero_tile(E* c, int m, int n, int m0, int n0, int threads) {
+    const int rows = min(m - m0, kVgemmTileM), cols = min(n - n0, kVgemmTileN);
+    for (int e = threadIdx.x; e < rows * cols; e += threads)
+        c[(int64_t)(m0 + e / cols) * n + n0 + e % cols] = E(0);
+}
+
+__global__ __launch_bounds__(Cfg<kVgemmTileM>::kThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
+void k_vgemm_bf16(VgemmArgs va, const uint16_t* __restrict__ a, const uint16_t* __restrict__ b, uint16_t* c) {
+    static_assert(kVgemmTileN == BN, "vgemm tiles are the GEMM's 128 x 256 tiles");
+    extern __shared__ __attribute__((aligned(16))) uint16_t smem[];
+    if (!vgemm_ok(va, true)) return;
+    const int e = vgemm_entry(blockIdx.x);
+    if (e >= uni(va.status[1])) return;
+    const VgemmTile t = vgemm_tile(va, e);
+    uint16_t* cp = c + t.c_off;
+    if (t.k == 0) {
+        vgemm_zero_tile(cp, t.m, t.n, t.m0, t.n0, Cfg<kVgemmTileM>::kThreads);
+        return;
+    }
+    gemm_tile_bf16<kVgemmTileM, 0, false, false>(a + t.a_off, t.k, b + t.b_off, nullptr, nullptr, 0, cp, t.n, t.m,
+                                                 t.k, t.n, t.m0, t.n0, smem);
+}
+
+// fp32: the 128 x 256 tile as eight 64 x 64 sub-tiles of the fp32 GEMM.
+__global__ __launch_bounds__(256) void k_vgemm_f32(VgemmArgs va, const float* __restrict__ a,
+                                                    const float* __restrict__ b, float* c) {
+    if (!vgemm_ok(va, false)) return;
+    const int e = vgemm_entry(blockIdx.x);
+    if (e >= uni(va.status[1])) return;
+    const VgemmTile t = vgemm_tile(va, e);
+    for (int sub = 0; sub < (kVgemmTileM / 64) * (kVgemmTileN / 64); ++sub) {
+        const int sm = t.m0 + (sub % (kVgemmTileM / 64)) * 64, sn = t.n0 + (sub / (kVgemmTileM / 64)) * 64;
+        if (sm < t.m && sn < t.n)
+            gemm_tile_f32<0>(a + t.a_off, t.k, b + t.b_off, nullptr, nullptr, 0, c + t.c_off, t.n, t.m, t.k, t.n, sm, sn);
     }
 }
 
@@ -383,6 +513,30 @@ hipError_t launch_bf16_act(const void* x, int ldx, const void* w, const void* bi
 }
 
 }  // namespace
+
+hipError_t launch_vgemm(const VgemmView& p, int dtype, const void* a, int64_t a_cap, const void* b, int64_t b_cap,
+                        void* c, int64_t c_cap, hipStream_t s) {
+    if (p.tile_cap == 0) return hipSuccess;
+    const VgemmArgs va{p.dims, p.a_off, p.b_off, p.c_off, reinterpret_cast<const int4*>(p.tile_items), p.status,
+                       p.batch, a_cap, b_cap, c_cap};
+    const int64_t grid = (p.tile_cap + kVgemmGridQuantum - 1) / kVgemmGridQuantum * kVgemmGridQuantum;
+    if (dtype == 1) {
+        using C = Cfg<kVgemmTileM>;
+        static bool attr_set = false;  // benign race: every thread sets the same value
+        if (!attr_set) {
+            hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_vgemm_bf16),
+                                               hipFuncAttributeMaxDynamicSharedMemorySize, C::kLdsBytes);
+            if (e != hipSuccess) return e;
+            attr_set = true;
+        }
+        hipLaunchKernelGGL(k_vgemm_bf16, dim3((unsigned)grid), dim3(C::kThreads), C::kLdsBytes, s, va,
+                           static_cast<const uint16_t*>(a), static_cast<const uint16_t*>(b), static_cast<uint16_t*>(c));
+    } else {
+        hipLaunchKernelGGL(k_vgemm_f32, dim3((unsigned)grid), dim3(256), 0, s, va, static_cast<const float*>(a),
+                           static_cast<const float*>(b), static_cast<float*>(c));
+    }
+    return hipGetLastError();
+}
 
 hipError_t launch_linear(int dtype, const void* x, int ldx, const void* w, const void* bias, const void* residual,
                          int ldr, int act, void* y, int ldy, int T, int K, int N, hipStream_t s) {

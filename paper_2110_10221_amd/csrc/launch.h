@@ -45,6 +45,24 @@ hipError_t launch_linear(int dtype, const void* x, int ldx, const void* w, const
                          const void* residual, int ldr, int act, void* y, int ldy, int T, int K, int N,
                          hipStream_t s);
 
+// Variable-sized batched GEMM.  VgemmView mirrors rag_vgemm_plan.
+struct VgemmView {
+    int32_t batch;
+    int64_t tile_cap;
+    const int32_t* dims;
+    int64_t* a_off;
+    int64_t* b_off;
+    int64_t* c_off;
+    int32_t* order;
+    int64_t* tile_off;
+    int32_t* tile_items;
+    int32_t* status;
+};
+
+hipError_t launch_vgemm_offsets(const VgemmView& p, hipStream_t s);
+hipError_t launch_vgemm(const VgemmView& p, int dtype, const void* a, int64_t a_cap, const void* b, int64_t b_cap,
+                        void* c, int64_t c_cap, hipStream_t s);
+
 hipError_t launch_layernorm(int dtype, const void* x, int ldx, const void* gamma, const void* beta,
                             float eps, void* y, int ldy, int T, int d, hipStream_t s);
 

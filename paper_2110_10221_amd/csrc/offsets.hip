@@ -277,7 +277,144 @@ __global__ __launch_bounds__(256) void k_plan_fill(const int32_t* __restrict__ l
     for (int t = threadIdx.x; t < L; t += 256) tok_seq[t0 + t] = b;
 }
 
+// ---------------------------------------------------------------------------
+// Variable-sized batched GEMM prelude: packed-storage offsets, largest-first
+// order, tile prefix and the flat tile list, in four launches like the plan
+// above (scan, rank, tile scan, fill).
+// ---------------------------------------------------------------------------
+
+// Sizes as the offsets count them: negative ones are flagged and counted as 0,
+// oversized ones flagged and clamped (so no sum can overflow).
+__device__ __forceinline__ int64_t vgemm_dim(int v) { return v < 0 ? 0 : (v > kVgemmMaxDim ? kVgemmMaxDim : v); }
+
+__global__ __launch_bounds__(kScanThreads) void k_vgemm_scan(const int32_t* __restrict__ dims, int B,
+                                                              int64_t* __restrict__ a_off,
+                                                              int64_t* __restrict__ b_off,
+                                                              int64_t* __restrict__ c_off,
+                                                              int32_t* __restrict__ status) {
+    __shared__ int64_t sh_a[kScanWaves], sh_b[kScanWaves];
+    __shared__ int sh_flags, sh_shape;
+    if (threadIdx.x == 0) {
+        sh_flags = 0;
+        sh_shape = 0;
+    }
+    __syncthreads();
+    int flags = 0, shape = 0;
+    int64_t carry_a = 0, carry_b = 0, carry_c = 0;
+    for (int base = 0; base < B; base += kScanThreads) {
+        const int p = base + threadIdx.x;
+        int64_t m = 0, n = 0, k = 0;
+        if (p < B) {
+            const int dm = dims[3 * p], dn = dims[3 * p + 1], dk = dims[3 * p + 2];
+            if (dm < 0 || dn < 0 || dk < 0) flags |= kVgemmNegSize;
+            if (dm > kVgemmMaxDim || dn > kVgemmMaxDim || dk > kVgemmMaxDim) flags |= kVgemmLargeSize;
+            if (dk % 64 != 0 || dn % 8 != 0) shape = 1;
+            m = vgemm_dim(dm);
+            n = vgemm_dim(dn);
+            k = vgemm_dim(dk);
+        }
+        int64_t ea, eb, ta, tb, ec, unused, tc, tu;
+        block_exclusive_scan2(m * k, n * k, ea, eb, ta, tb, sh_a, sh_b);
+        block_exclusive_scan2(m * n, 0, ec, unused, tc, tu, sh_a, sh_b);
+        if (p < B) {
+            a_off[p] = carry_a + ea;
+            b_off[p] = carry_b + eb;
+            c_off[p] = carry_c + ec;
+        }
+        carry_a += ta;
+        carry_b += tb;
+        carry_c += tc;
+    }
+    if (flags) atomicOr(&sh_flags, flags);
+    if (shape) atomicOr(&sh_shape, shape);
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        a_off[B] = carry_a;
+        b_off[B] = carry_b;
+        c_off[B] = carry_c;
+        status[0] = sh_flags;
+        status[1] = 0;
+        status[2] = sh_shape;
+    }
+}
+
+// Same strict total order as k_plan_rank, on the multiply-add count m n k.
+__global__ __launch_bounds__(256) void k_vgemm_rank(const int32_t* __restrict__ dims, int B,
+                                                     int32_t* __restrict__ order) {
+    __shared__ int64_t ws[256];
+    const int p = blockIdx.x * 256 + threadIdx.x;
+    const int64_t wp = p < B ? vgemm_dim(dims[3 * p]) * vgemm_dim(dims[3 * p + 1]) * vgemm_dim(dims[3 * p + 2]) : 0;
+    int rank = 0;
+    for (int base = 0; base < B; base += 256) {
+        __syncthreads();
+        const int q = base + threadIdx.x;
+        ws[threadIdx.x] = q < B ? vgemm_dim(dims[3 * q]) * vgemm_dim(dims[3 * q + 1]) * vgemm_dim(dims[3 * q + 2]) : 0;
+        __syncthreads();
+        const int n = min(256, B - base);
+        for (int j = 0; j < n; ++j) {
+            const int64_t wq = ws[j];
+            rank += (wq > wp) | ((wq == wp) & (base + j < p));
+        }
+    }
+    if (p < B) order[rank] = p;
+}
+
+__device__ __forceinline__ int64_t vgemm_tiles(const int32_t* dims, int p) {
+    return ((vgemm_dim(dims[3 * p]) + kVgemmTileM - 1) / kVgemmTileM) *
+           ((vgemm_dim(dims[3 * p + 1]) + kVgemmTileN - 1) / kVgemmTileN);
+}
+
+__global__ __launch_bounds__(kScanThreads) void k_vgemm_tile_scan(const int32_t* __restrict__ dims,
+                                                                   const int32_t* __restrict__ order, int B,
+                                                                   int64_t tile_cap,
+                                                                   int64_t* __restrict__ tile_off,
+                                                                   int32_t* __restrict__ status) {
+    __shared__ int64_t sh_a[kScanWaves], sh_b[kScanWaves];
+    int64_t carry = 0;
+    for (int base = 0; base < B; base += kScanThreads) {
+        const int r = base + threadIdx.x;
+        const int64_t nt = r < B ? vgemm_tiles(dims, order[r]) : 0;
+        int64_t e, unused, t, tu;
+        block_exclusive_scan2(nt, 0, e, unused, t, tu, sh_a, sh_b);
+        if (r < B) tile_off[r] = carry + e;
+        carry += t;
+    }
+    if (threadIdx.x == 0) {
+        int f = status[0];
+        if (carry > tile_cap) f |= kVgemmTileCap;
+        tile_off[B] = carry;
+        status[0] = f;
+        status[1] = f ? 0 : static_cast<int32_t>(carry);
+    }
+}
+
+// Workgroup r writes the tiles of the r-th largest problem, tile rows fastest.
+__global__ __launch_bounds__(256) void k_vgemm_fill(const int32_t* __restrict__ dims,
+                                                     const int32_t* __restrict__ order,
+                                                     const int64_t* __restrict__ tile_off,
+                                                     int32_t* __restrict__ tile_items,
+                                                     const int32_t* __restrict__ status) {
+    if (status[0] != 0) return;
+    const int r = blockIdx.x;
+    const int p = order[r];
+    const int tm = static_cast<int>((vgemm_dim(dims[3 * p]) + kVgemmTileM - 1) / kVgemmTileM);
+    const int n = static_cast<int>(tile_off[r + 1] - tile_off[r]);
+    int4* out = reinterpret_cast<int4*>(tile_items) + tile_off[r];
+    for (int idx = threadIdx.x; idx < n; idx += 256) out[idx] = make_int4(p, idx % tm, idx / tm, 0);
+}
+
 }  // namespace
+
+hipError_t launch_vgemm_offsets(const VgemmView& p, hipStream_t s) {
+    hipLaunchKernelGGL(k_vgemm_scan, dim3(1), dim3(kScanThreads), 0, s, p.dims, p.batch, p.a_off, p.b_off, p.c_off,
+                       p.status);
+    hipLaunchKernelGGL(k_vgemm_rank, dim3((p.batch + 255) / 256), dim3(256), 0, s, p.dims, p.batch, p.order);
+    hipLaunchKernelGGL(k_vgemm_tile_scan, dim3(1), dim3(kScanThreads), 0, s, p.dims, p.order, p.batch, p.tile_cap,
+                       p.tile_off, p.status);
+    hipLaunchKernelGGL(k_vgemm_fill, dim3(p.batch), dim3(256), 0, s, p.dims, p.order, p.tile_off, p.tile_items,
+                       p.status);
+    return hipGetLastError();
+}
 
 hipError_t launch_offsets(const PlanView& p, hipStream_t s) {
     if (p.batch <= kScanThreads) {

@@ -161,3 +161,56 @@ def test_host_validation_rejects_bad_arguments():
     assert b"overlap" in lib.ragged_last_error()
     lib.ragged_status_string.restype = ctypes.c_char_p
     assert lib.ragged_status_string(-5) == b"RAG_ERR_WORKSPACE"
+
+
+def _vplan(rag, **over):
+    f = dict(batch=3, tile_cap=40, dims=FAKE, a_off=FAKE + 0x1000, b_off=FAKE + 0x2000, c_off=FAKE + 0x3000,
+             order=FAKE + 0x4000, tile_off=FAKE + 0x5000, tile_items=FAKE + 0x6000, status=FAKE + 0x7000)
+    f.update(over)
+    return rag.RagVgemmPlan(**f)
+
+
+@needs_lib
+def test_vgemm_plan_struct_and_capacity():
+    import numpy as np
+    import paper_2110_10221_amd as rag
+
+    # int32 batch (padded to 8) + int64 tile_cap + 8 pointers
+    assert ctypes.sizeof(rag.RagVgemmPlan) == 8 + 8 + 8 * 8
+    rng = np.random.default_rng(0)
+    dims = rng.integers(0, 3000, size=(50, 3)).astype(np.int32)
+    cap = rag.vgemm_plan_capacity(50, int(dims[:, 0].max()), int(dims[:, 1].max()))
+    assert int(oracle.vgemm_offsets(dims).tile_off[-1]) <= cap
+    assert rag.vgemm_plan_capacity(2, 129, 256) == 2 * 2 * 1
+    with pytest.raises(rag.RaggedError, match="RAG_ERR_ARG"):
+        rag.vgemm_plan_capacity(0, 128, 128)
+
+
+@needs_lib
+@no_gpu
+def test_vgemm_host_validation():
+    import paper_2110_10221_amd as rag
+
+    lib = rag.library()
+    P = ctypes.c_void_p
+    ERR_ARG, ERR_DTYPE, ERR_SHAPE, ERR_CAP = -1, -2, -3, -4
+    s = None
+    off = lib.vgemm_offsets
+    assert off(None, s) == ERR_ARG
+    assert off(ctypes.byref(_vplan(rag, batch=0)), s) == ERR_ARG
+    assert off(ctypes.byref(_vplan(rag, batch=4097)), s) == ERR_ARG
+    assert off(ctypes.byref(_vplan(rag, tile_cap=-1)), s) == ERR_ARG
+    assert off(ctypes.byref(_vplan(rag, tile_cap=(1 << 30) + 1)), s) == ERR_CAP
+    assert off(ctypes.byref(_vplan(rag, order=0)), s) == ERR_ARG
+    assert off(ctypes.byref(_vplan(rag, tile_items=FAKE + 8)), s) == ERR_ARG    # not 16-byte aligned
+    assert off(ctypes.byref(_vplan(rag, a_off=FAKE + 4)), s) == ERR_ARG         # int64 array misaligned
+    plan = ctypes.byref(_vplan(rag))
+    a, b, c = P(FAKE + 0x100000), P(FAKE + 0x200000), P(FAKE + 0x300000)
+    vg = lib.ragged_vgemm
+    vg.argtypes = [P, P, ctypes.c_int64, P, ctypes.c_int64, P, ctypes.c_int64, ctypes.c_int32, P]
+    assert vg(plan, a, 10, b, 10, c, 10, 5, s) == ERR_DTYPE
+    assert vg(plan, None, 10, b, 10, c, 10, 1, s) == ERR_ARG
+    assert vg(plan, a, -1, b, 10, c, 10, 1, s) == ERR_ARG
+    assert vg(plan, P(FAKE + 0x100008), 10, b, 10, c, 10, 1, s) == ERR_SHAPE      # bf16 needs 16-byte alignment
+    assert vg(plan, a, 10, b, 10, P(FAKE + 0x100010), 10, 1, s) == ERR_ARG        # c overlaps a
+    assert vg(plan, a, 10, b, 10, P(FAKE + 0x200000 + 36), 100, 0, s) == ERR_ARG  # c overlaps b (fp32)

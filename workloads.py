@@ -184,3 +184,24 @@ def make_workload(cid: int, seed: int = 0, lengths: np.ndarray | None = None,
 def random_storage(rng: np.random.Generator, shape, dtype: str, scale: float = 1.0) -> np.ndarray:
     """A standalone seeded N(0, scale^2) tensor in storage form."""
     return as_storage(rng.standard_normal(shape) * scale, dtype)
+
+
+# ---------------------------------------------------------------------------
+# Variable-sized batched GEMM (the paper's matrix-multiplication experiment,
+# Section 7.1): every m, n and k drawn uniformly from the multiples of 128 in
+# [512, 1408]; operands N(0, 1), packed one problem after another.
+# ---------------------------------------------------------------------------
+VGEMM_DIM_CHOICES = np.arange(512, 1408 + 1, 128)
+
+
+def draw_vgemm_dims(batch: int, rng: np.random.Generator) -> np.ndarray:
+    """[batch, 3] int32 (m, n, k), each uniform over VGEMM_DIM_CHOICES."""
+    return rng.choice(VGEMM_DIM_CHOICES, size=(batch, 3)).astype(np.int32)
+
+
+def make_vgemm_operands(dims, rng: np.random.Generator, dtype: str, scale: float = 1.0):
+    """Packed A (sum m k elements) and B (sum n k elements) storage arrays."""
+    d = np.asarray(dims, np.int64).reshape(-1, 3)
+    a = random_storage(rng, (int((d[:, 0] * d[:, 2]).sum()),), dtype, scale)
+    b = random_storage(rng, (int((d[:, 1] * d[:, 2]).sum()),), dtype, scale)
+    return a, b
