@@ -62,6 +62,7 @@ def lib():
         l.oracle_vgemm_offsets.restype = ctypes.c_int
         l.oracle_vgemm_offsets.argtypes = [i32, p, i32, i32, p, p, p, p, p]
         l.oracle_vgemm.argtypes = [ctypes.c_int, i32, p, p, p, p]
+        l.oracle_trmm.argtypes = [ctypes.c_int, i32, i32, p, i64, p, i64, p, i64]
         _lib = l
     return _lib
 
@@ -228,3 +229,17 @@ def vgemm(dtype, dims, a, b):
     lib().oracle_vgemm(_DT[dtype], d.shape[0], _ptr(d), _ptr(np.ascontiguousarray(a)), _ptr(np.ascontiguousarray(b)),
                        _ptr(c))
     return c[:c_elems]
+
+
+def trmm(dtype, n: int, m: int, l, b, ldl: int | None = None, ldb: int | None = None):
+    """C = tril(L) B for L [n, n] (leading dimension ldl, entries above the
+    diagonal ignored) and B [n, m] (ldb); returns C [n, m] in storage form."""
+    ldl = n if ldl is None else ldl
+    ldb = m if ldb is None else ldb
+    l = np.ascontiguousarray(l).reshape(-1)
+    b = np.ascontiguousarray(b).reshape(-1)
+    if n > 0 and (l.size < (n - 1) * ldl + n or (m > 0 and b.size < (n - 1) * ldb + m)):
+        raise ValueError("operand smaller than its declared shape")
+    c = np.zeros((n, m), _storage_dtype(dtype))
+    lib().oracle_trmm(_DT[dtype], n, m, _ptr(l), ldl, _ptr(b), ldb, _ptr(c), m)
+    return c

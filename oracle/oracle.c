@@ -497,3 +497,26 @@ void oracle_vgemm(int dtype, int32_t B, const int32_t* dims, const void* a, cons
         co += m * n;
     }
 }
+
+/* ------------------------------------------------------------------------ */
+/* Triangular matrix multiplication (trmm, Section 7.1)                      */
+/* ------------------------------------------------------------------------ */
+
+/*
+ * trmm: a square lower-triangular matrix L (n x n) times a dense matrix B
+ * (n x m).  Row i of a triangular matrix holds its nonzeros in columns 0..i,
+ * so the reduction over k is a variable loop whose extent depends on the
+ * output row (the paper's vloop):
+ *   C[i][j] = rd(sum_{k <= i} L[i][k] * B[k][j]),   i < n, j < m.
+ * Entries of L above the diagonal are never read.  All three are row-major
+ * with leading dimensions ldl, ldb, ldc.
+ */
+void oracle_trmm(int dtype, int32_t n, int32_t m, const void* l, int64_t ldl, const void* b, int64_t ldb, void* c,
+                 int64_t ldc) {
+    for (int64_t i = 0; i < n; ++i)
+        for (int64_t j = 0; j < m; ++j) {
+            double acc = 0.0;
+            for (int64_t k = 0; k <= i; ++k) acc += load(l, dtype, i * ldl + k) * load(b, dtype, k * ldb + j);
+            store(c, dtype, i * ldc + j, acc);
+        }
+}
