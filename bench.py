@@ -313,6 +313,40 @@ def vgemm_measurement(rag, batch=128, iters=20):
                     "at the batch's largest m, n, k)"}
 
 
+def trmm_measurement(rag, n=8192, m=8192, iters=20):
+    """Triangular matrix multiplication (the paper's trmm experiment): C = tril(L) B
+    with L n x n and B n x m in bf16, against the dense product of the same
+    (zero-filled) triangle with torch.matmul, the fully padded GEMM the paper
+    compares with.  Useful FLOPs: m n (n + 1) (the k <= i multiply-adds)."""
+    import torch
+
+    g = torch.Generator(device="cuda").manual_seed(3)
+    L = torch.randn(n, n, device="cuda", generator=g).bfloat16().tril_()
+    B = torch.randn(n, m, device="cuda", generator=g).bfloat16()
+    C = torch.empty(n, m, device="cuda", dtype=torch.bfloat16)
+
+    def timed(fn):
+        for _ in range(3):
+            fn()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(iters):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / iters
+
+    ms = timed(lambda: rag.ragged_trmm(L, B, C))
+    ms_dense = timed(lambda: torch.matmul(L, B, out=C))
+    useful = float(m) * n * (n + 1)
+    tf = useful / (ms * 1e-3) / 1e12
+    return {"workload": f"trmm, lower-triangular {n} x {n} times dense {n} x {m}, bf16",
+            "ms": round(ms, 4), "useful_tflops": round(tf, 1), "frac_of_bf16_peak": round(tf / PEAK_BF16_TFLOPS, 4),
+            "kernel": "k_trmm_bf16", "dense_matmul_ms": round(ms_dense, 4),
+            "speedup_vs_dense_matmul": round(ms_dense / ms, 3),
+            "note": "dense stand-in: torch.matmul (hipBLASLt) of the zero-filled triangle, 2 n^2 m FLOPs"}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -324,6 +358,7 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-masked", action="store_true", help="skip the masked (causal) attention measurement")
     ap.add_argument("--no-vgemm", action="store_true", help="skip the variable-sized batched GEMM measurement")
+    ap.add_argument("--no-trmm", action="store_true", help="skip the triangular matrix multiplication measurement")
     ap.add_argument("--cpu-target-flops", type=float, default=2.0e10)
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of MIB MiB five times (counter calibration) and exit")
@@ -472,6 +507,8 @@ def main():
         out["masked"] = masked_measurement(rag, plan, wl, x, wstruct, ws, y, args.flags)
     if not args.no_vgemm:
         out["vgemm"] = vgemm_measurement(rag)
+    if not args.no_trmm:
+        out["trmm"] = trmm_measurement(rag)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(wl, args.cpu_target_flops)
     else:

@@ -350,6 +350,24 @@ rag_status vgemm_offsets(rag_vgemm_plan* plan, void* stream);
 rag_status ragged_vgemm(const rag_vgemm_plan* plan, const void* a, int64_t a_cap, const void* b,
                         int64_t b_cap, void* c, int64_t c_cap, int32_t dtype, void* stream);
 
+/*
+ * Triangular matrix multiplication (trmm; Section 7.1, the matrix-multiplication
+ * experiments): a square lower-triangular L times a dense B,
+ *   C[i][j] = sum_{k <= i} L[i][k] * B[k][j],   i < n, j < m,
+ * L [n, n] (ldl >= n), B [n, m] (ldb >= m), C [n, m] (ldc >= m), all row-major.
+ * Row i of L holds its nonzeros in columns 0..i, so the reduction is a
+ * variable loop whose extent grows with the row; entries above the diagonal
+ * never reach the result (they may hold anything, NaN included).  Output row
+ * tiles with the most work run first.  dtype RAG_BF16 (fp32 accumulation,
+ * rounded to nearest even when stored) needs m, ldl, ldb and ldc to be
+ * multiples of 8, 16-byte aligned operands, (n + 64) * ldb < 2^30 and
+ * ldl < 2^23; RAG_F32 takes
+ * any sizes.  C must not overlap L or B.  With n == 0 or m == 0 nothing is
+ * accessed.
+ */
+rag_status ragged_trmm(const void* l, int32_t ldl, const void* b, int32_t ldb, void* c, int32_t ldc, int32_t n,
+                       int32_t m, int32_t dtype, void* stream);
+
 /* encoder_layer flags */
 enum {
     RAG_LAYER_UNFUSED_ATTENTION = 1, /* run ragged_qkt/softmax/attn_v with a

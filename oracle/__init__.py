@@ -63,6 +63,7 @@ def lib():
         l.oracle_vgemm_offsets.argtypes = [i32, p, i32, i32, p, p, p, p, p]
         l.oracle_vgemm.argtypes = [ctypes.c_int, i32, p, p, p, p]
         l.oracle_trmm.argtypes = [ctypes.c_int, i32, i32, p, i64, p, i64, p, i64]
+        l.oracle_trmm_rows.argtypes = [ctypes.c_int, i32, p, i64, p, i64, p, i32, p, i64]
         _lib = l
     return _lib
 
@@ -242,4 +243,18 @@ def trmm(dtype, n: int, m: int, l, b, ldl: int | None = None, ldb: int | None = 
         raise ValueError("operand smaller than its declared shape")
     c = np.zeros((n, m), _storage_dtype(dtype))
     lib().oracle_trmm(_DT[dtype], n, m, _ptr(l), ldl, _ptr(b), ldb, _ptr(c), m)
+    return c
+
+
+def trmm_rows(dtype, n: int, m: int, l, b, rows, ldl: int | None = None, ldb: int | None = None):
+    """Rows `rows` of tril(L) B (same arguments as trmm); returns [len(rows), m]."""
+    ldl = n if ldl is None else ldl
+    ldb = m if ldb is None else ldb
+    r = np.ascontiguousarray(rows, np.int32)
+    if r.size and (r.min() < 0 or r.max() >= n):
+        raise ValueError("row out of range")
+    l = np.ascontiguousarray(l).reshape(-1)
+    b = np.ascontiguousarray(b).reshape(-1)
+    c = np.zeros((r.size, m), _storage_dtype(dtype))
+    lib().oracle_trmm_rows(_DT[dtype], m, _ptr(l), ldl, _ptr(b), ldb, _ptr(r), r.size, _ptr(c), m)
     return c

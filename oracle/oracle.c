@@ -520,3 +520,17 @@ void oracle_trmm(int dtype, int32_t n, int32_t m, const void* l, int64_t ldl, co
             store(c, dtype, i * ldc + j, acc);
         }
 }
+
+/* The same definition for selected output rows only: row rows[r] of C goes to
+ * row r of c (for spot checks of large products). */
+void oracle_trmm_rows(int dtype, int32_t m, const void* l, int64_t ldl, const void* b, int64_t ldb,
+                      const int32_t* rows, int32_t nrows, void* c, int64_t ldc) {
+    for (int32_t r = 0; r < nrows; ++r) {
+        const int64_t i = rows[r];
+        for (int64_t j = 0; j < m; ++j) {
+            double acc = 0.0;
+            for (int64_t k = 0; k <= i; ++k) acc += load(l, dtype, i * ldl + k) * load(b, dtype, k * ldb + j);
+            store(c, dtype, r * ldc + j, acc);
+        }
+    }
+}

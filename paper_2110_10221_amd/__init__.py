@@ -89,6 +89,7 @@ _c_layernorm = _sig("packed_layernorm", [_p, _i32, _p, _p, _f32, _p, _i32, _i32,
 _c_vgemm_capacity = _sig("vgemm_plan_capacity", [_i32, _i32, _i32, ctypes.POINTER(_i64)])
 _c_vgemm_offsets = _sig("vgemm_offsets", [ctypes.POINTER(RagVgemmPlan), _p])
 _c_vgemm = _sig("ragged_vgemm", [ctypes.POINTER(RagVgemmPlan), _p, _i64, _p, _i64, _p, _i64, _i32, _p])
+_c_trmm = _sig("ragged_trmm", [_p, _i32, _p, _i32, _p, _i32, _i32, _i32, _i32, _p])
 _c_ws = _sig("encoder_layer_workspace", [_i32, _i32, _i32, _i32, _i32, _i32, _i32, ctypes.POINTER(ctypes.c_size_t)])
 _c_layer = _sig("encoder_layer", [ctypes.POINTER(RagPlan), _p, _p, _i32, _i32, _i32, _i32, _f32, _i32, _i32,
                                   ctypes.POINTER(RagLayerWeights), _p, ctypes.c_size_t, _i32, _p, _p])
@@ -340,3 +341,15 @@ def ragged_vgemm(plan: VgemmPlan, a, b, c, stream=None):
             raise ValueError("a, b and c must be contiguous")
     _check("ragged_vgemm", _c_vgemm(plan.ref(), _ptr(a), a.numel(), _ptr(b), b.numel(), _ptr(c), c.numel(),
                                     _dtype_code(a), _stream(stream)))
+
+
+def ragged_trmm(l, b, c, stream=None):
+    """C = tril(L) B: l [n, n], b and c [n, m], 2-D tensors of one dtype with unit
+    column stride (entries of l above the diagonal are ignored)."""
+    n, m = b.shape
+    if l.shape[0] != n or l.shape[1] < n or c.shape != b.shape:
+        raise ValueError("expected l [n, n], b [n, m] and c [n, m]")
+    if not (l.dtype == b.dtype == c.dtype):
+        raise TypeError("l, b and c must share one dtype")
+    _check("ragged_trmm", _c_trmm(_ptr(l), _ld(l), _ptr(b), _ld(b), _ptr(c), _ld(c), n, m, _dtype_code(b),
+                                  _stream(stream)))

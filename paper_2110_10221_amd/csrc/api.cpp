@@ -535,4 +535,27 @@ rag_status ragged_vgemm(const rag_vgemm_plan* plan, const void* a, int64_t a_cap
     return finish(rag::launch_vgemm(v, dtype, a, a_cap, b, b_cap, c, c_cap, s), s, plan->status, fn);
 }
 
+rag_status ragged_trmm(const void* l, int32_t ldl, const void* b, int32_t ldb, void* c, int32_t ldc, int32_t n,
+                       int32_t m, int32_t dtype, void* stream) {
+    const char* fn = "ragged_trmm";
+    rag_status st;
+    if ((st = check_dtype(dtype, fn))) return st;
+    if (n < 0 || m < 0) return fail(RAG_ERR_ARG, "%s: negative size (n %d, m %d)", fn, n, m);
+    if (n == 0 || m == 0) return RAG_OK;
+    if ((st = check_operand(l, ldl, n, dtype, 16, "L", fn)) || (st = check_operand(b, ldb, m, dtype, 16, "B", fn)) ||
+        (st = check_operand(c, ldc, m, dtype, 16, "C", fn)))
+        return st;
+    if (dtype == RAG_BF16) {
+        if (m % 8 != 0) return fail(RAG_ERR_SHAPE, "%s: bf16 needs m %% 8 == 0 (m = %d)", fn, m);
+        // 32-bit buffer offsets: B rows up to n rounded to 64, 128-row panels of L
+        if ((int64_t)(n + 64) * ldb >= (int64_t)1 << 30 || ldl >= 1 << 23)
+            return fail(RAG_ERR_SHAPE, "%s: bf16 needs (n + 64) * ldb < 2^30 and ldl < 2^23", fn);
+    }
+    const size_t lc = span_bytes(n, ldc, m, dtype);
+    if (ranges_overlap(c, lc, l, span_bytes(n, ldl, n, dtype)) || ranges_overlap(c, lc, b, span_bytes(n, ldb, m, dtype)))
+        return fail(RAG_ERR_ARG, "%s: C overlaps L or B", fn);
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    return finish(rag::launch_trmm(dtype, l, ldl, b, ldb, c, ldc, n, m, s), s, nullptr, fn);
+}
+
 }  // extern "C"

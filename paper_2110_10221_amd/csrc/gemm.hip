@@ -98,6 +98,28 @@ __device__ __forceinline__ bf16x8 lds_frag(const uint16_t* tile, int row, int ch
     return as_bf16x8(*reinterpret_cast<const u32x4*>(tile + row * BK + ((chunk ^ swz(row)) * 8)));
 }
 
+// w operand stored [K][N] (N contiguous; the dense right factor of trmm): an LDS
+// stage holds BK rows of BN columns, 512-byte rows of kKnChunks 16-byte chunks
+// whose index is XOR-swizzled by (row & 3) << 2.  The transposed fragment reads
+// below take rows r..r+3 (64 bytes each per half-wave), which the swizzle puts
+// on four distinct 64-byte bank segments.
+constexpr int kKnChunks = BN / 8;
+constexpr int kKnRowsPerBlock = 64 / kKnChunks;  // rows one 1 KB wave copy fills
+__device__ __forceinline__ int swz_kn(int row) { return (row & 3) << 2; }
+
+typedef __attribute__((ext_vector_type(4))) short short4_t;
+typedef __attribute__((address_space(3))) short4_t lds_short4_t;
+
+// ds_read_b64_tr_b16: within each 16-lane group, lane 4e + q supplies the
+// address of row e, columns 4q..4q+3 of a 4 x 16 block; lane t of the group
+// receives column t of rows 0..3.  Two such reads (rows +0..3 and +4..7) give a
+// lane eight consecutive k of one column: the MFMA operand layout.
+__device__ __forceinline__ bf16x8 lds_frag_tr(const uint16_t* lo_addr, const uint16_t* hi_addr) {
+    const u32x2 lo = __builtin_bit_cast(u32x2, __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_short4_t*)lo_addr));
+    const u32x2 hi = __builtin_bit_cast(u32x2, __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_short4_t*)hi_addr));
+    return as_bf16x8(u32x4{lo[0], lo[1], hi[0], hi[1]});
+}
+
 // Output tile of a linear workgroup id.  Workgroups are dealt to the 8 XCDs
 // round-robin, so the id is first remapped to give each XCD a contiguous range.
 // That range is walked in groups of kGroupM token tiles, token tile fastest, so
@@ -128,12 +150,19 @@ __device__ __forceinline__ void wait_copies(int n) {
 
 // One BM x BN output tile at (m0, n0) of y = act(x w^T + bias) + residual, w being
 // [N, K] with K contiguous; smem holds Cfg<BM>::kLdsBytes.  Called by the workgroup
-// as a whole (it synchronises on LDS).
-template <int BM, int ACT, bool HAS_BIAS, bool HAS_RES>
+// as a whole (it synchronises on LDS).  K (a multiple of 64) is the extent of the
+// reduction the tile runs.
+//   W_KN  w is instead [K rows][N] with leading dimension ldw and kvalid valid
+//         rows (rows past it read as zeros): y = x w.
+//   TRI   x is lower triangular: x[i][k] counts only for k <= i.  The K steps
+//         wholly below the tile's first row run unchecked; the others zero the
+//         fragment entries with k > i after reading them (operation splitting of
+//         the reduction loop's last iterations, Section 4).
+template <int BM, int ACT, bool HAS_BIAS, bool HAS_RES, bool W_KN = false, bool TRI = false>
 __device__ __forceinline__ void gemm_tile_bf16(const uint16_t* __restrict__ x, int ldx, const uint16_t* __restrict__ w,
                                                const uint16_t* __restrict__ bias, const uint16_t* residual, int ldr,
                                                uint16_t* y, int ldy, int T, int K, int N, int m0, int n0,
-                                               uint16_t* smem) {
+                                               uint16_t* smem, int ldw = 0, int kvalid = 0) {
     using C = Cfg<BM>;
     constexpr int kStages = C::kStages, kStageElems = C::kStageElems, kCopies = C::kCopies;
     const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
@@ -141,12 +170,23 @@ __device__ __forceinline__ void gemm_tile_bf16(const uint16_t* __restrict__ x, i
     const int l32 = lane % 32, h2 = lane / 32;
 
     const __amdgpu_buffer_rsrc_t rx = make_rsrc(x + (int64_t)m0 * ldx, (uint32_t)min(T - m0, BM) * ldx * 2u);
-    const __amdgpu_buffer_rsrc_t rw = make_rsrc(w + (int64_t)n0 * K, (uint32_t)min(N - n0, BN) * K * 2u);
+    __amdgpu_buffer_rsrc_t rw;
+    if constexpr (W_KN)  // through the last valid column of the last valid row
+        rw = make_rsrc(w + n0, kvalid > 0 ? (uint32_t)(((int64_t)(kvalid - 1) * ldw + min(N - n0, BN)) * 2) : 0u);
+    else
+        rw = make_rsrc(w + (int64_t)n0 * K, (uint32_t)min(N - n0, BN) * K * 2u);
     int vx[C::kXBlocks], vw[C::kWBlocks];
 #pragma unroll
     for (int i = 0; i < C::kXBlocks; ++i) vx[i] = copy_voffset(lane, (wave * C::kXBlocks + i) * kRowsPerBlock, ldx * 2);
 #pragma unroll
-    for (int i = 0; i < C::kWBlocks; ++i) vw[i] = copy_voffset(lane, (wave * C::kWBlocks + i) * kRowsPerBlock, K * 2);
+    for (int i = 0; i < C::kWBlocks; ++i) {
+        if constexpr (W_KN) {  // lane l fills slot l of rows 2 blk, 2 blk + 1 (physical chunk l % 32)
+            const int row = (wave * C::kWBlocks + i) * kKnRowsPerBlock + lane / kKnChunks;
+            vw[i] = row * ldw * 2 + ((lane % kKnChunks) ^ swz_kn(row)) * 16;
+        } else {
+            vw[i] = copy_voffset(lane, (wave * C::kWBlocks + i) * kRowsPerBlock, K * 2);
+        }
+    }
     auto issue = [&](int step) {
         uint16_t* xs = smem + (step % kStages) * kStageElems;
         uint16_t* ws = xs + BM * BK;
@@ -154,8 +194,25 @@ __device__ __forceinline__ void gemm_tile_bf16(const uint16_t* __restrict__ x, i
 #pragma unroll
         for (int i = 0; i < C::kXBlocks; ++i) copy_block(rx, xs + (wave * C::kXBlocks + i) * 512, vx[i], k0b);
 #pragma unroll
-        for (int i = 0; i < C::kWBlocks; ++i) copy_block(rw, ws + (wave * C::kWBlocks + i) * 512, vw[i], k0b);
+        for (int i = 0; i < C::kWBlocks; ++i) {
+            if constexpr (W_KN)  // the step moves down the rows: keep it in the range-checked offset
+                copy_block(rw, ws + (wave * C::kWBlocks + i) * 512, vw[i] + step * BK * ldw * 2, 0);
+            else
+                copy_block(rw, ws + (wave * C::kWBlocks + i) * 512, vw[i], k0b);
+        }
     };
+    // transposed-read addresses of the [K][N] layout: rows 8 h2 + e (+4), columns
+    // wn*WN + i*32 + 16 (g & 1) + 4q, g = lane / 16 (so the lane's column is l32)
+    int tr_row = 0, tr_col[FN];
+    if constexpr (W_KN) {
+        const int e = (lane % 16) / 4, q = lane % 4, g = lane / 16;
+        tr_row = (8 * h2 + e) * BN;
+#pragma unroll
+        for (int i = 0; i < FN; ++i) {
+            const int col = wn * WN + i * 32 + 16 * (g & 1) + 4 * q;
+            tr_col[i] = (((col >> 3) ^ swz_kn(e)) << 3) + (col & 7);
+        }
+    }
 
     floatx16 acc[FN][FM];
 #pragma unroll
@@ -174,16 +231,35 @@ __device__ __forceinline__ void gemm_tile_bf16(const uint16_t* __restrict__ x, i
 #pragma unroll
             for (int j = 0; j < FM; ++j) fb[ks][j] = lds_frag(xb, wm * WM + j * 32 + l32, ks * 2 + h2);
     };
+    // TRI edge steps: zero the x entries with k > i of a landed stage in LDS, then
+    // a barrier (the stage is read only after it).  In registers the masks would
+    // push the loop past the register budget.
+    auto mask_x = [&](int step) {
+        uint32_t* xs = reinterpret_cast<uint32_t*>(smem + (step % kStages) * kStageElems);
+        constexpr int kDwords = BM * BK / 2, kPerRow = BK / 2;
+#pragma unroll
+        for (int d = threadIdx.x; d < kDwords; d += C::kThreads) {
+            const int r = d / kPerRow, p = d % kPerRow;
+            const int k = step * BK + (((p / 4) ^ swz(r)) * 8) + (p % 4) * 2;  // the dword's first k
+            const int i = m0 + r;
+            if (k + 1 > i) xs[d] = k > i ? 0u : (xs[d] & 0x0000ffffu);
+        }
+        barrier_lds();
+    };
     auto read_w1 = [&](bf16x8 (&fa)[KSTEPS][FN], int step, int ks, int i) {
         const uint16_t* wb = smem + (step % kStages) * kStageElems + BM * BK;
-        fa[ks][i] = lds_frag(wb, wn * WN + i * 32 + l32, ks * 2 + h2);
+        if constexpr (W_KN)
+            fa[ks][i] = lds_frag_tr(wb + tr_row + ks * 16 * BN + tr_col[i], wb + tr_row + (ks * 16 + 4) * BN + tr_col[i]);
+        else
+            fa[ks][i] = lds_frag(wb, wn * WN + i * 32 + l32, ks * 2 + h2);
     };
     // one K step with a successor: prefetch its fragments while the MFMAs run
     auto step_next = [&](bf16x8 (&fa)[KSTEPS][FN], bf16x8 (&fb)[KSTEPS][FM], bf16x8 (&na)[KSTEPS][FN],
-                         bf16x8 (&nb)[KSTEPS][FM], int kt, int nk) {
+                         bf16x8 (&nb)[KSTEPS][FM], int kt, int nk, auto masked) {
         wait_copies<kCopies>(min(kStages - 2, nk - 2 - kt) * kCopies);
         barrier_lds();  // step kt+1's stage is visible; step kt's stage is no longer read
         if (kt + kStages < nk) issue(kt + kStages);
+        if constexpr (decltype(masked)::value) mask_x(kt + 1);
         read_x(nb, kt + 1);
 #pragma unroll
         for (int ks = 0; ks < KSTEPS; ++ks)
@@ -204,22 +280,35 @@ __device__ __forceinline__ void gemm_tile_bf16(const uint16_t* __restrict__ x, i
     };
 
     const int nk = K / BK;
+    // TRI: steps below kfree have every k under the tile's first row (no check);
+    // the rest form the separately compiled edge loop
+    const int kfree = TRI ? min(m0 / BK, nk) : nk;
+    constexpr std::bool_constant<false> plain{};
+    constexpr std::bool_constant<TRI> edge{};
 #pragma unroll
     for (int st = 0; st < kStages; ++st)
         if (st < nk) issue(st);
     wait_copies<kCopies>(min(kStages - 1, nk - 1) * kCopies);
     barrier_lds();
+    if (TRI && kfree == 0) mask_x(0);
     read_x(fb0, 0);
 #pragma unroll
     for (int ks = 0; ks < KSTEPS; ++ks)
 #pragma unroll
         for (int i = 0; i < FN; ++i) read_w1(fa0, 0, ks, i);
     // K is a multiple of 64, so nk = K / 32 is even: steps pair up with one exit path
-    for (int kt = 0; kt + 2 < nk; kt += 2) {
-        step_next(fa0, fb0, fa1, fb1, kt, nk);
-        step_next(fa1, fb1, fa0, fb0, kt + 1, nk);
+    int kt = 0;
+    for (; kt + 2 < nk && kt + 2 < kfree; kt += 2) {
+        step_next(fa0, fb0, fa1, fb1, kt, nk, plain);
+        step_next(fa1, fb1, fa0, fb0, kt + 1, nk, plain);
     }
-    step_next(fa0, fb0, fa1, fb1, nk - 2, nk);
+    if constexpr (TRI) {
+        for (; kt + 2 < nk; kt += 2) {
+            step_next(fa0, fb0, fa1, fb1, kt, nk, edge);
+            step_next(fa1, fb1, fa0, fb0, kt + 1, nk, edge);
+        }
+    }
+    step_next(fa0, fb0, fa1, fb1, nk - 2, nk, edge);
     step_last(fa1, fb1);
 
     // Epilogue through LDS, 32 tokens at a time: the waves holding a slice write
@@ -470,6 +559,103 @@ __global__ __launch_bounds__(256) void k_vgemm_f32(VgemmArgs va, const float* __
     }
 }
 
+// ---------------------------------------------------------------------------
+// Triangular matrix multiplication C = tril(L) B (trmm; Section 7.1): L is
+// n x n, B and C are n x m, all row-major.  The reduction over k is a variable
+// loop (k <= i), so the output row tile tm needs k < min(128 (tm + 1), n) only:
+// tile work grows with tm.  The tiles run heaviest first (thread remapping,
+// Section 4), dealt to the XCDs by row tile: XCD x takes row tiles in a snake
+// over blocks of eight (top-down x, then 7 - x, ...), which gives every XCD the
+// same total work when the tile rows fill whole blocks of 16, and walks its
+// tiles in groups of kTrmmGroup row tiles, row tile fastest, so the tiles it
+// runs together share both L and B panels in its L2.
+// ---------------------------------------------------------------------------
+constexpr int kTrmmTile = 128;  // output rows per tile (the BM = 128 GEMM tile)
+constexpr int kTrmmGroup = 4;
+
+// Row tile of local panel r of XCD x (heaviest first), or -1.
+__device__ __forceinline__ int trmm_panel(int tiles_m, int xcd, int r) {
+    const int pos = (r & 1) ? 7 - xcd : xcd;
+    const int tm = tiles_m - 1 - (8 * r + pos);
+    return tm;
+}
+
+__device__ __forceinline__ int trmm_local_panels(int tiles_m, int xcd) {
+    const int full = tiles_m / 8, rem = tiles_m % 8;
+    const int pos = (full & 1) ? 7 - xcd : xcd;
+    return full + (pos < rem ? 1 : 0);
+}
+
+// False if this workgroup has no tile (the grid is rounded up per XCD).
+__device__ __forceinline__ bool trmm_tile_coords(int bid, int tiles_m, int tiles_n, int& tm, int& tn) {
+    const int xcd = bid % 8, idx = bid / 8;
+    const int n_local = trmm_local_panels(tiles_m, xcd);
+    if (idx >= n_local * tiles_n) return false;
+    const int gsz = kTrmmGroup * tiles_n, first = (idx / gsz) * kTrmmGroup;
+    const int gr = min(n_local - first, kTrmmGroup);
+    const int r = first + (idx % gsz) % gr;
+    tn = (idx % gsz) / gr;
+    tm = trmm_panel(tiles_m, xcd, r);
+    return true;
+}
+
+__global__ __launch_bounds__(Cfg<kTrmmTile>::kThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
+void k_trmm_bf16(const uint16_t* __restrict__ l, int ldl, const uint16_t* __restrict__ b, int ldb, uint16_t* c,
+                 int ldc, int n, int m, int tiles_m, int tiles_n) {
+    extern __shared__ __attribute__((aligned(16))) uint16_t smem[];
+    int tm, tn;
+    if (!trmm_tile_coords(blockIdx.x, tiles_m, tiles_n, tm, tn)) return;
+    const int m0 = tm * kTrmmTile;
+    const int k_end = min(m0 + kTrmmTile, (n + 63) & ~63);  // a multiple of 64; L and B past n read as zeros
+    gemm_tile_bf16<kTrmmTile, 0, false, false, true, true>(l, ldl, b, nullptr, nullptr, 0, c, ldc, n, k_end, m, m0,
+                                                            tn * BN, smem, ldb, n);
+}
+
+// fp32: 64 x 64 tiles of plain FMA, the reduction stopping at the tile's last row
+// and L entries past the diagonal read as zero.
+__global__ __launch_bounds__(256) void k_trmm_f32(const float* __restrict__ l, int ldl, const float* __restrict__ b,
+                                                   int ldb, float* c, int ldc, int n, int m) {
+    __shared__ float ls[16][64 + 1], bs[16][64 + 1];
+    const int tiles_m = (n + 63) / 64;
+    const int m0 = (tiles_m - 1 - (int)blockIdx.x) * 64, n0 = blockIdx.y * 64;  // heaviest rows first
+    const int tx = threadIdx.x % 16, ty = threadIdx.x / 16;
+    const int k_end = min(m0 + 64, n);
+    float acc[4][4] = {};
+    for (int k0 = 0; k0 < k_end; k0 += 16) {
+        __syncthreads();
+        for (int e = threadIdx.x; e < 64 * 16; e += 256) {
+            const int r = e / 16, cc = e % 16, k = k0 + cc;
+            ls[cc][r] = (m0 + r < n && k <= m0 + r) ? l[(int64_t)(m0 + r) * ldl + k] : 0.f;
+            const int kr = k0 + e / 64, col = n0 + e % 64;
+            bs[e / 64][e % 64] = (kr < n && col < m) ? b[(int64_t)kr * ldb + col] : 0.f;
+        }
+        __syncthreads();
+#pragma unroll
+        for (int cc = 0; cc < 16; ++cc) {
+            float av[4], bv[4];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                av[u] = ls[cc][ty * 4 + u];
+                bv[u] = bs[cc][tx + 16 * u];
+            }
+#pragma unroll
+            for (int u = 0; u < 4; ++u)
+#pragma unroll
+                for (int v = 0; v < 4; ++v) acc[u][v] = fmaf(av[u], bv[v], acc[u][v]);
+        }
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+        const int i = m0 + ty * 4 + u;
+        if (i >= n) continue;
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+            const int j = n0 + tx + 16 * v;
+            if (j < m) c[(int64_t)i * ldc + j] = acc[u][v];
+        }
+    }
+}
+
 template <int BM, int ACT, bool HB, bool HR>
 hipError_t launch_bf16_tiles(const void* x, int ldx, const void* w, const void* bias, const void* residual, int ldr,
                              void* y, int ldy, int T, int K, int N, hipStream_t s) {
@@ -534,6 +720,31 @@ hipError_t launch_vgemm(const VgemmView& p, int dtype, const void* a, int64_t a_
     } else {
         hipLaunchKernelGGL(k_vgemm_f32, dim3((unsigned)grid), dim3(256), 0, s, va, static_cast<const float*>(a),
                            static_cast<const float*>(b), static_cast<float*>(c));
+    }
+    return hipGetLastError();
+}
+
+hipError_t launch_trmm(int dtype, const void* l, int ldl, const void* b, int ldb, void* c, int ldc, int n, int m,
+                       hipStream_t s) {
+    if (n == 0 || m == 0) return hipSuccess;
+    if (dtype == 1) {
+        using C = Cfg<kTrmmTile>;
+        const int tiles_m = (n + kTrmmTile - 1) / kTrmmTile, tiles_n = (m + BN - 1) / BN;
+        const int per_xcd = (tiles_m + 7) / 8 * tiles_n;  // most tiles any XCD takes
+        static bool attr_set = false;  // benign race: every thread sets the same value
+        if (!attr_set) {
+            hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_trmm_bf16),
+                                               hipFuncAttributeMaxDynamicSharedMemorySize, C::kLdsBytes);
+            if (e != hipSuccess) return e;
+            attr_set = true;
+        }
+        hipLaunchKernelGGL(k_trmm_bf16, dim3(8 * per_xcd), dim3(C::kThreads), C::kLdsBytes, s,
+                           static_cast<const uint16_t*>(l), ldl, static_cast<const uint16_t*>(b), ldb,
+                           static_cast<uint16_t*>(c), ldc, n, m, tiles_m, tiles_n);
+    } else {
+        hipLaunchKernelGGL(k_trmm_f32, dim3((n + 63) / 64, (m + 63) / 64), dim3(256), 0, s,
+                           static_cast<const float*>(l), ldl, static_cast<const float*>(b), ldb, static_cast<float*>(c),
+                           ldc, n, m);
     }
     return hipGetLastError();
 }

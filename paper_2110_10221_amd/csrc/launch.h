@@ -63,6 +63,10 @@ hipError_t launch_vgemm_offsets(const VgemmView& p, hipStream_t s);
 hipError_t launch_vgemm(const VgemmView& p, int dtype, const void* a, int64_t a_cap, const void* b, int64_t b_cap,
                         void* c, int64_t c_cap, hipStream_t s);
 
+// C = tril(L) B: L [n, n] (ldl), B and C [n, m] (ldb, ldc).
+hipError_t launch_trmm(int dtype, const void* l, int ldl, const void* b, int ldb, void* c, int ldc, int n, int m,
+                       hipStream_t s);
+
 hipError_t launch_layernorm(int dtype, const void* x, int ldx, const void* gamma, const void* beta,
                             float eps, void* y, int ldy, int T, int d, hipStream_t s);
 

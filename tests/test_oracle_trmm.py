@@ -78,3 +78,12 @@ def test_brute_force_and_leading_dimensions():
 def test_empty_shapes():
     assert oracle.trmm(F32, 0, 5, np.zeros(0, np.float32), np.zeros(0, np.float32)).shape == (0, 5)
     assert oracle.trmm(F32, 3, 0, np.ones(9, np.float32), np.zeros(0, np.float32), ldb=1).shape == (3, 0)
+
+
+def test_selected_rows_equal_the_full_product():
+    rng = np.random.default_rng(11)
+    n, m = 70, 19
+    L, B = _ops(rng, n, m, BF16)
+    full = oracle.trmm(BF16, n, m, L, B)
+    rows = [0, 1, 33, 69, 33]
+    assert np.array_equal(oracle.trmm_rows(BF16, n, m, L, B, rows), full[rows])

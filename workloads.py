@@ -205,3 +205,16 @@ def make_vgemm_operands(dims, rng: np.random.Generator, dtype: str, scale: float
     a = random_storage(rng, (int((d[:, 0] * d[:, 2]).sum()),), dtype, scale)
     b = random_storage(rng, (int((d[:, 1] * d[:, 2]).sum()),), dtype, scale)
     return a, b
+
+
+# ---------------------------------------------------------------------------
+# Triangular matrix multiplication (Section 7.1): a square lower-triangular L
+# and a dense B, entries N(0, 1); the strict upper triangle of L's storage is
+# filled with NaN so that any read of it shows in the result.
+# ---------------------------------------------------------------------------
+def make_trmm_operands(n: int, m: int, rng: np.random.Generator, dtype: str, nan_upper: bool = True):
+    """L [n, n] and B [n, m] storage arrays."""
+    lv = rng.standard_normal((n, n))
+    if nan_upper:
+        lv[np.triu_indices(n, 1)] = np.nan
+    return as_storage(lv, dtype), as_storage(rng.standard_normal((n, m)), dtype)
