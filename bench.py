@@ -55,6 +55,8 @@ KERNEL_SOURCES = {
     "k_gemm_bf16": "paper_2110_10221_amd/csrc/gemm.hip",
     "k_attention_bf16": "paper_2110_10221_amd/csrc/attention.hip",
     "k_layernorm": "paper_2110_10221_amd/csrc/layernorm.hip",
+    "k_vgemm_bf16": "paper_2110_10221_amd/csrc/gemm.hip",
+    "k_trmm_bf16": "paper_2110_10221_amd/csrc/gemm.hip",
 }
 
 
@@ -303,9 +305,11 @@ def vgemm_measurement(rag, batch=128, iters=20):
 
     ms_loop = timed(per_problem)
     tf = useful / (ms * 1e-3) / 1e12
+    alg_bytes = 2.0 * (a_n + b_n + c_n)
     return {"workload": f"vgemm, batch {batch}, m n k uniform over multiples of 128 in [512, 1408] (seed {batch})",
             "ms": round(ms, 4), "useful_tflops": round(tf, 1), "frac_of_bf16_peak": round(tf / PEAK_BF16_TFLOPS, 4),
             "kernel": "k_vgemm_bf16", "tiles": plan.n_tiles(), "plan_ms": round(ms_plan, 4),
+            "algorithmic_bytes": alg_bytes, "hbm_bytes_per_launch": load_traffic("k_vgemm_bf16"),
             "padded_bmm_ms": round(ms_pad, 4), "speedup_vs_padded_bmm": round(ms_pad / ms, 3),
             "per_problem_matmul_ms": round(ms_loop, 4), "speedup_vs_per_problem_matmul": round(ms_loop / ms, 3),
             "useful_fraction_of_padded": round(useful / (2.0 * batch * M * N * K), 4),
@@ -343,6 +347,7 @@ def trmm_measurement(rag, n=8192, m=8192, iters=20):
     return {"workload": f"trmm, lower-triangular {n} x {n} times dense {n} x {m}, bf16",
             "ms": round(ms, 4), "useful_tflops": round(tf, 1), "frac_of_bf16_peak": round(tf / PEAK_BF16_TFLOPS, 4),
             "kernel": "k_trmm_bf16", "dense_matmul_ms": round(ms_dense, 4),
+            "algorithmic_bytes": 2.0 * (n * (n + 1) / 2 + 2.0 * n * m), "hbm_bytes_per_launch": load_traffic("k_trmm_bf16"),
             "speedup_vs_dense_matmul": round(ms_dense / ms, 3),
             "note": "dense stand-in: torch.matmul (hipBLASLt) of the zero-filled triangle, 2 n^2 m FLOPs"}
 
