@@ -212,6 +212,28 @@ def derive_traffic(fetch_csv, write_csv, cal_fetch_csv, cal_write_csv, copy_mib)
     print(json.dumps(out, indent=1, sort_keys=True))
 
 
+def _timed(fn, iters=20, warm_ms=150.0):
+    """Mean ms per call of fn on the current stream: fn runs untimed until the GPU has
+    been busy for warm_ms (its clock ramps up over the first tens of ms of load),
+    then `iters` calls are timed with events."""
+    import torch
+
+    t0 = time.perf_counter()
+    n = 0
+    while n < 5 or (time.perf_counter() - t0) * 1e3 < warm_ms:
+        fn()
+        n += 1
+        if n % 5 == 0:
+            torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(iters):
+        fn()
+    e1.record()
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) / iters
+
+
 def masked_measurement(rag, plan, wl, x, wstruct, ws, y, flags, iters=20):
     """Masked (causal) attention on the same batch: the fused kernel with and without the
     mask on packed Q, K, V of the layer's shape, and the masked layer.  Useful FLOPs of
@@ -226,16 +248,7 @@ def masked_measurement(rag, plan, wl, x, wstruct, ws, y, flags, iters=20):
     o = torch.empty(T, d, device="cuda", dtype=torch.bfloat16)
     scale = 1.0 / math.sqrt(64)
 
-    def timed(fn):
-        for _ in range(3):
-            fn()
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record()
-        for _ in range(iters):
-            fn()
-        e1.record()
-        torch.cuda.synchronize()
-        return e0.elapsed_time(e1) / iters
+    timed = lambda fn: _timed(fn, iters)
 
     rag.ragged_offsets(plan)
     ms_full = timed(lambda: rag.ragged_attention(plan, q, k, v, o, scale))
@@ -273,16 +286,7 @@ def vgemm_measurement(rag, batch=128, iters=20):
     plan = rag.VgemmPlan(torch.from_numpy(dims).cuda(), host_dims=dims)
     rag.vgemm_offsets(plan)
 
-    def timed(fn):
-        for _ in range(3):
-            fn()
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record()
-        for _ in range(iters):
-            fn()
-        e1.record()
-        torch.cuda.synchronize()
-        return e0.elapsed_time(e1) / iters
+    timed = lambda fn: _timed(fn, iters)
 
     ms = timed(lambda: rag.ragged_vgemm(plan, a, b, c))
     assert not plan.data_errors(), plan.data_errors()
@@ -329,16 +333,7 @@ def trmm_measurement(rag, n=8192, m=8192, iters=20):
     B = torch.randn(n, m, device="cuda", generator=g).bfloat16()
     C = torch.empty(n, m, device="cuda", dtype=torch.bfloat16)
 
-    def timed(fn):
-        for _ in range(3):
-            fn()
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record()
-        for _ in range(iters):
-            fn()
-        e1.record()
-        torch.cuda.synchronize()
-        return e0.elapsed_time(e1) / iters
+    timed = lambda fn: _timed(fn, iters)
 
     ms = timed(lambda: rag.ragged_trmm(L, B, C))
     ms_dense = timed(lambda: torch.matmul(L, B, out=C))
@@ -356,7 +351,8 @@ def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
-    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=200,
+                    help="untimed steps first (the GPU clock needs tens of ms of load to settle)")
     ap.add_argument("--config", type=int, default=4)
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--flags", type=int, default=0, help="encoder_layer flags (1 = unfused attention)")
