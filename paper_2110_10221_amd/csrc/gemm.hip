@@ -453,7 +453,10 @@ __global__ __launch_bounds__(256) void k_gemm_f32(const float* __restrict__ x, i
 // problem and share its operand panels in that XCD's L2, while every XCD still
 // gets a share of the large problems first.
 // ---------------------------------------------------------------------------
-constexpr int kVgemmChunk = 16;
+#ifndef RAG_VGEMM_CHUNK
+#define RAG_VGEMM_CHUNK 32
+#endif
+constexpr int kVgemmChunk = RAG_VGEMM_CHUNK;
 constexpr int kVgemmGridQuantum = 8 * kVgemmChunk;  // the grid is a multiple of this
 
 struct VgemmArgs {
@@ -564,38 +567,22 @@ __global__ __launch_bounds__(256) void k_vgemm_f32(VgemmArgs va, const float* __
 // n x n, B and C are n x m, all row-major.  The reduction over k is a variable
 // loop (k <= i), so the output row tile tm needs k < min(128 (tm + 1), n) only:
 // tile work grows with tm.  The tiles run heaviest first (thread remapping,
-// Section 4), dealt to the XCDs by row tile: XCD x takes row tiles in a snake
-// over blocks of eight (top-down x, then 7 - x, ...), which gives every XCD the
-// same total work when the tile rows fill whole blocks of 16, and walks its
-// tiles in groups of kTrmmGroup row tiles, row tile fastest, so the tiles it
-// runs together share both L and B panels in its L2.
+// Section 4).
 // ---------------------------------------------------------------------------
 constexpr int kTrmmTile = 128;  // output rows per tile (the BM = 128 GEMM tile)
-constexpr int kTrmmGroup = 4;
 
-// Row tile of local panel r of XCD x (heaviest first), or -1.
-__device__ __forceinline__ int trmm_panel(int tiles_m, int xcd, int r) {
-    const int pos = (r & 1) ? 7 - xcd : xcd;
-    const int tm = tiles_m - 1 - (8 * r + pos);
-    return tm;
-}
 
-__device__ __forceinline__ int trmm_local_panels(int tiles_m, int xcd) {
-    const int full = tiles_m / 8, rem = tiles_m % 8;
-    const int pos = (full & 1) ? 7 - xcd : xcd;
-    return full + (pos < rem ? 1 : 0);
-}
-
-// False if this workgroup has no tile (the grid is rounded up per XCD).
-__device__ __forceinline__ bool trmm_tile_coords(int bid, int tiles_m, int tiles_n, int& tm, int& tn) {
+// Tiles are listed heaviest row first, columns ascending, and dealt to the XCDs
+// in chunks of `chunk` consecutive columns (workgroups go to the XCDs
+// round-robin).  With chunk = tiles_n / 8 each XCD owns the same column panels
+// of B in every row (so B is fetched into one L2, not eight) and gets the same
+// share of every row, hence the same total work.
+__device__ __forceinline__ bool trmm_tile_coords(int bid, int tiles_m, int tiles_n, int chunk, int& tm, int& tn) {
     const int xcd = bid % 8, idx = bid / 8;
-    const int n_local = trmm_local_panels(tiles_m, xcd);
-    if (idx >= n_local * tiles_n) return false;
-    const int gsz = kTrmmGroup * tiles_n, first = (idx / gsz) * kTrmmGroup;
-    const int gr = min(n_local - first, kTrmmGroup);
-    const int r = first + (idx % gsz) % gr;
-    tn = (idx % gsz) / gr;
-    tm = trmm_panel(tiles_m, xcd, r);
+    const int t = ((idx / chunk) * 8 + xcd) * chunk + idx % chunk;
+    if (t >= tiles_m * tiles_n) return false;
+    tm = tiles_m - 1 - t / tiles_n;
+    tn = t % tiles_n;
     return true;
 }
 
@@ -604,7 +591,7 @@ void k_trmm_bf16(const uint16_t* __restrict__ l, int ldl, const uint16_t* __rest
                  int ldc, int n, int m, int tiles_m, int tiles_n) {
     extern __shared__ __attribute__((aligned(16))) uint16_t smem[];
     int tm, tn;
-    if (!trmm_tile_coords(blockIdx.x, tiles_m, tiles_n, tm, tn)) return;
+    if (!trmm_tile_coords(blockIdx.x, tiles_m, tiles_n, max(1, tiles_n / 8), tm, tn)) return;
     const int m0 = tm * kTrmmTile;
     const int k_end = min(m0 + kTrmmTile, (n + 63) & ~63);  // a multiple of 64; L and B past n read as zeros
     gemm_tile_bf16<kTrmmTile, 0, false, false, true, true>(l, ldl, b, nullptr, nullptr, 0, c, ldc, n, k_end, m, m0,
@@ -730,7 +717,8 @@ hipError_t launch_trmm(int dtype, const void* l, int ldl, const void* b, int ldb
     if (dtype == 1) {
         using C = Cfg<kTrmmTile>;
         const int tiles_m = (n + kTrmmTile - 1) / kTrmmTile, tiles_n = (m + BN - 1) / BN;
-        const int per_xcd = (tiles_m + 7) / 8 * tiles_n;  // most tiles any XCD takes
+        const int q = 8 * max(1, tiles_n / 8);  // the grid covers whole rounds of chunks
+        const int per_xcd = (tiles_m * tiles_n + q - 1) / q * q / 8;
         static bool attr_set = false;  // benign race: every thread sets the same value
         if (!attr_set) {
             hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_trmm_bf16),
