@@ -27,6 +27,12 @@
 //    lane ends with four consecutive output features of one token.  The fp32
 //    results pass through LDS in 32-token slices so that bias / activation /
 //    residual are applied while whole 512-byte rows move to and from memory.
+//
+// The same tile body (gemm_tile_bf16) also serves the variable-sized batched
+// GEMM (one workgroup per entry of a plan's tile list, Section 7.1) and the
+// triangular product C = tril(L) B (a [K][N] right operand read through
+// transposing LDS loads, and a triangular left operand whose last K steps are
+// masked), both further down.
 #include <type_traits>
 
 #include "device_common.h"

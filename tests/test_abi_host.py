@@ -214,3 +214,32 @@ def test_vgemm_host_validation():
     assert vg(plan, P(FAKE + 0x100008), 10, b, 10, c, 10, 1, s) == ERR_SHAPE      # bf16 needs 16-byte alignment
     assert vg(plan, a, 10, b, 10, P(FAKE + 0x100010), 10, 1, s) == ERR_ARG        # c overlaps a
     assert vg(plan, a, 10, b, 10, P(FAKE + 0x200000 + 36), 100, 0, s) == ERR_ARG  # c overlaps b (fp32)
+
+
+@needs_lib
+@no_gpu
+def test_trmm_host_validation():
+    import paper_2110_10221_amd as rag
+
+    lib = rag.library()
+    P = ctypes.c_void_p
+    ERR_ARG, ERR_DTYPE, ERR_SHAPE = -1, -2, -3
+    tr = lib.ragged_trmm
+    tr.argtypes = [P, ctypes.c_int32, P, ctypes.c_int32, P, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
+                   ctypes.c_int32, P]
+    l, b, c = P(FAKE), P(FAKE + 0x10000000), P(FAKE + 0x20000000)
+    s = None
+    assert tr(l, 64, b, 64, c, 64, 64, 64, 4, s) == ERR_DTYPE
+    assert tr(l, 64, b, 64, c, 64, -1, 64, 1, s) == ERR_ARG
+    assert tr(l, 64, b, 64, c, 64, 0, 64, 1, s) == 0            # empty: nothing to do, nothing launched
+    assert tr(l, 64, b, 64, c, 64, 64, 0, 1, s) == 0
+    assert tr(l, 32, b, 64, c, 64, 64, 64, 1, s) == ERR_SHAPE    # ldl < n
+    assert tr(l, 64, b, 60, c, 64, 64, 64, 1, s) == ERR_SHAPE    # ldb < m
+    assert tr(l, 64, b, 72, c, 72, 64, 68, 1, s) == ERR_SHAPE    # bf16: m % 8
+    assert tr(l, 68, b, 64, c, 64, 64, 64, 1, s) == ERR_SHAPE    # bf16: ld keeps rows 16-byte aligned
+    assert tr(P(FAKE + 8), 64, b, 64, c, 64, 64, 64, 1, s) == ERR_SHAPE   # misaligned bf16 operand
+    assert tr(None, 64, b, 64, c, 64, 64, 64, 1, s) == ERR_ARG
+    assert tr(l, 64, b, 64, P(FAKE + 0x10000000 + 64), 64, 64, 64, 1, s) == ERR_ARG   # C overlaps B
+    assert tr(l, 64, b, 64, P(FAKE + 4096), 64, 64, 64, 1, s) == ERR_ARG             # C overlaps L
+    assert tr(l, 1 << 23, b, 64, c, 64, 64, 64, 1, s) == ERR_SHAPE                    # ldl too large for bf16
+    assert b"ldl" in lib.ragged_last_error()
