@@ -264,6 +264,62 @@ def masked_measurement(rag, plan, wl, x, wstruct, ws, y, flags, iters=20):
             "note": "fused causal attention and the masked layer (plan included once, not per call)"}
 
 
+def sdpa_measurement(rag, cid, seed=0, iters=30):
+    """The unfused ragged attention operators one by one (ragged_offsets,
+    ragged_qkt, ragged_softmax, ragged_attn_v; bf16, scale 1/8) on configuration
+    `cid`'s lengths and shape, each against its own roofline: the prelude and the
+    softmax as algorithmic bytes / time against HBM, QK^T and Attn.V as useful
+    FLOPs / time against bf16 MFMA peak (their bytes are reported too: the score
+    buffer makes them HBM-heavy)."""
+    import torch
+
+    from tests.helpers import dev
+    from workloads import CONFIGS, make_workload
+
+    cfg = CONFIGS[cid]
+    wl = make_workload(cid, seed=seed)
+    L = wl.lengths.astype(np.int64)
+    T, d, H = wl.total_tokens, cfg.d_model, cfg.heads
+    s2 = float((L * L).sum())
+    plan = rag.Plan(torch.from_numpy(wl.lengths).cuda(), T, cfg.max_len, H)
+    if cfg.kind == "sdpa":
+        q, k, v = (dev(wl.tensors[n], "bf16").view(T, d) for n in ("q", "k", "v"))
+    else:
+        g = torch.Generator(device="cuda").manual_seed(1)
+        q, k, v = (torch.randn(T, d, device="cuda", generator=g).bfloat16() for _ in range(3))
+    n_s = int(H * s2)
+    S = torch.empty(n_s, dtype=torch.bfloat16, device="cuda")
+    P = torch.empty_like(S)
+    O = torch.empty(T, d, dtype=torch.bfloat16, device="cuda")
+    rag.ragged_offsets(plan)
+    torch.cuda.synchronize()
+    n_qkt, n_av = int(plan.status[1].item()), int(plan.status[2].item())
+    ms_off = _timed(lambda: rag.ragged_offsets(plan), iters)
+    ms_qkt = _timed(lambda: rag.ragged_qkt(plan, q, k, S, 0.125), iters)
+    ms_sm = _timed(lambda: rag.ragged_softmax(plan, S, P), iters)
+    ms_av = _timed(lambda: rag.ragged_attn_v(plan, P, v, O), iters)
+    assert not plan.data_errors(), plan.data_errors()
+    e = 2.0
+    B = len(L)  # lengths in; tok_off, att_off, order, two item prefixes, tok_seq, items, status out
+    by = {"offsets": 4.0 * B + 4.0 * (B + 1) + 8.0 * (B + 1) + 4.0 * B + 8.0 * (B + 1) + 4.0 * T + 16.0 * n_qkt
+                     + 12.0 * n_av + 16.0,
+          "qkt": e * (2 * T * d + H * s2), "softmax": e * 2 * H * s2, "attn_v": e * (H * s2 + 2 * T * d)}
+    fl = {"qkt": 2.0 * d * s2, "attn_v": 2.0 * d * s2}
+    ms = {"offsets": ms_off, "qkt": ms_qkt, "softmax": ms_sm, "attn_v": ms_av}
+    ops = {}
+    for n, t in ms.items():
+        o = {"ms": round(t, 5), "algorithmic_bytes": by[n], "GB_per_s": round(by[n] / (t * 1e-3) / 1e9, 1),
+             "frac_of_hbm_peak": round(by[n] / (t * 1e-3) / 1e9 / PEAK_HBM_GBS, 4)}
+        if n in fl:
+            o["useful_tflops"] = round(fl[n] / (t * 1e-3) / 1e12, 1)
+            o["frac_of_bf16_peak"] = round(fl[n] / (t * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4)
+        ops[n] = o
+    return {"workload": f"config {cid}: batch {cfg.batch}, lengths {cfg.lengths.replace(':', ' ')}, {H} heads x 64, bf16, "
+                        f"T = {T}, {n_s} scores", "ops": ops,
+            "kernels": {"offsets": "k_plan_small + k_plan_fill" if len(L) <= 1024 else "k_plan_scan/rank/items/fill",
+                        "qkt": "k_qkt_bf16", "softmax": "k_softmax<true>", "attn_v": "k_attn_v_bf16"}}
+
+
 def vgemm_measurement(rag, batch=128, iters=20):
     """Variable-sized batched GEMM (the paper's matrix-multiplication experiment):
     `batch` problems with m, n, k uniform over the multiples of 128 in [512, 1408],
@@ -360,6 +416,7 @@ def main():
     ap.add_argument("--no-masked", action="store_true", help="skip the masked (causal) attention measurement")
     ap.add_argument("--no-vgemm", action="store_true", help="skip the variable-sized batched GEMM measurement")
     ap.add_argument("--no-trmm", action="store_true", help="skip the triangular matrix multiplication measurement")
+    ap.add_argument("--no-sdpa", action="store_true", help="skip the unfused attention operator measurements")
     ap.add_argument("--cpu-target-flops", type=float, default=2.0e10)
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of MIB MiB five times (counter calibration) and exit")
@@ -506,6 +563,8 @@ def main():
     }
     if not args.no_masked:
         out["masked"] = masked_measurement(rag, plan, wl, x, wstruct, ws, y, args.flags)
+    if not args.no_sdpa:
+        out["sdpa_unfused"] = {"sdpa_b32": sdpa_measurement(rag, 2), "layer_b128": sdpa_measurement(rag, 4)}
     if not args.no_vgemm:
         out["vgemm"] = vgemm_measurement(rag)
     if not args.no_trmm:

@@ -56,49 +56,55 @@ __device__ __forceinline__ u32x4 ld16(const uint16_t* p) { return *reinterpret_c
 
 constexpr int kStage = kTile + 8;  // padded LDS row (elements)
 
+// One item per (sequence, head, 64-query block) from the Attn.V work list: the
+// block's Q fragments are loaded once and the item walks every key tile of the
+// row, so the 128-byte pieces of each score row are written back to back by one
+// workgroup (the L2 can merge them into whole lines before they reach HBM).
 __global__ __launch_bounds__(256) void k_qkt_bf16(PlanArgs pa, const uint16_t* __restrict__ q, int ldq,
                                                    const uint16_t* __restrict__ k, int ldk, float scale,
                                                    uint16_t* __restrict__ S, int64_t score_cap, int causal) {
     if (!plan_ok(pa, score_cap)) return;
     __shared__ uint16_t tile[kTile][kStage];
-    const int n_items = pa.status[1];
+    const int n_items = pa.status[2];
     const int H = pa.heads;
     const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
     const int l16 = lane % 16, q4 = lane / 16;
     for (int it = blockIdx.x; it < n_items; it += gridDim.x) {
-        const int4 item = reinterpret_cast<const int4*>(pa.qkt_items)[it];
-        const int b = item.x, h = item.y, ti = item.z, tj = item.w;
-        if (causal && tj > ti) continue;  // masked: tiles above the diagonal hold no score
+        const int b = pa.av_items[3 * it], h = pa.av_items[3 * it + 1], ti = pa.av_items[3 * it + 2];
         const int L = pa.lengths[b];
         const int t0 = pa.tok_off[b];
         const int64_t base = pa.att_off[b];
-        // this wave: query rows ti*64 + wave*16 .. +15, all 64 key columns of the tile
+        // this wave: query rows ti*64 + wave*16 .. +15
         const int qi = min(ti * kTile + wave * 16 + l16, L - 1);
         const uint16_t* qrow = q + (int64_t)(t0 + qi) * ldq + h * kHeadDim + 8 * q4;
         const bf16x8 qa0 = as_bf16x8(ld16(qrow)), qa1 = as_bf16x8(ld16(qrow + 32));
-        floatx4 acc[4];
+        const int rows = min(kTile, L - ti * kTile);
+        const int n_tj = causal ? ti + 1 : (L + kTile - 1) / kTile;  // masked: key tiles up to the diagonal
+        for (int tj = 0; tj < n_tj; ++tj) {
+            floatx4 acc[4];
 #pragma unroll
-        for (int jb = 0; jb < 4; ++jb) {
-            const int kj = min(tj * kTile + jb * 16 + l16, L - 1);
-            const uint16_t* krow = k + (int64_t)(t0 + kj) * ldk + h * kHeadDim + 8 * q4;
-            const bf16x8 kb0 = as_bf16x8(ld16(krow)), kb1 = as_bf16x8(ld16(krow + 32));
-            acc[jb] = floatx4{0.f, 0.f, 0.f, 0.f};
-            acc[jb] = mfma16x16x32(kb0, qa0, acc[jb]);  // C[j][i] = sum_c K[j][c] Q[i][c]
-            acc[jb] = mfma16x16x32(kb1, qa1, acc[jb]);
+            for (int jb = 0; jb < 4; ++jb) {
+                const int kj = min(tj * kTile + jb * 16 + l16, L - 1);
+                const uint16_t* krow = k + (int64_t)(t0 + kj) * ldk + h * kHeadDim + 8 * q4;
+                const bf16x8 kb0 = as_bf16x8(ld16(krow)), kb1 = as_bf16x8(ld16(krow + 32));
+                acc[jb] = floatx4{0.f, 0.f, 0.f, 0.f};
+                acc[jb] = mfma16x16x32(kb0, qa0, acc[jb]);  // C[j][i] = sum_c K[j][c] Q[i][c]
+                acc[jb] = mfma16x16x32(kb1, qa1, acc[jb]);
+            }
+            __syncthreads();  // the previous tile's stores have read the staging tile
+#pragma unroll
+            for (int jb = 0; jb < 4; ++jb)
+#pragma unroll
+                for (int r = 0; r < 4; ++r)
+                    tile[wave * 16 + l16][jb * 16 + 4 * q4 + r] = f32_to_bf16(acc[jb][r] * scale);
+            __syncthreads();
+            const int cols = min(kTile, L - tj * kTile);
+            // masked: only keys j <= i are written (the diagonal tile's upper part is left alone)
+            const int jmax = causal ? ti * kTile - tj * kTile : kTile;
+            for (int rr = wave; rr < rows; rr += 4)
+                if (lane < cols && lane <= jmax + rr)
+                    S[base + ((int64_t)(ti * kTile + rr) * H + h) * L + tj * kTile + lane] = tile[rr][lane];
         }
-        __syncthreads();  // the previous item's stores have read the staging tile
-#pragma unroll
-        for (int jb = 0; jb < 4; ++jb)
-#pragma unroll
-            for (int r = 0; r < 4; ++r)
-                tile[wave * 16 + l16][jb * 16 + 4 * q4 + r] = f32_to_bf16(acc[jb][r] * scale);
-        __syncthreads();
-        const int rows = min(kTile, L - ti * kTile), cols = min(kTile, L - tj * kTile);
-        // masked: only keys j <= i are written (the diagonal tile's upper part is left alone)
-        const int jmax = causal ? ti * kTile - tj * kTile : kTile;
-        for (int rr = wave; rr < rows; rr += 4)
-            if (lane < cols && lane <= jmax + rr)
-                S[base + ((int64_t)(ti * kTile + rr) * H + h) * L + tj * kTile + lane] = tile[rr][lane];
     }
 }
 
@@ -599,7 +605,7 @@ int persistent_grid(int64_t cap, int per_cu) {
 hipError_t launch_qkt(const PlanView& p, int dtype, const void* q, int ldq, const void* k, int ldk, float scale,
                       void* scores, int64_t score_cap, bool causal, hipStream_t s) {
     const PlanArgs pa = plan_args(p);
-    const int grid = persistent_grid(p.qkt_cap, 8);
+    const int grid = persistent_grid(dtype == 1 ? p.av_cap : p.qkt_cap, 8);
     if (dtype == 1)
         hipLaunchKernelGGL(k_qkt_bf16, dim3(grid), dim3(256), 0, s, pa, static_cast<const uint16_t*>(q), ldq,
                            static_cast<const uint16_t*>(k), ldk, scale, static_cast<uint16_t*>(scores), score_cap,
