@@ -61,7 +61,7 @@ def test_offsets_edge_cases(L, H):
     _check_equal(plan, np.asarray(L, np.int32), H)
 
 
-@pytest.mark.parametrize("B", [1023, 1024, 1025, 5000, 65536])
+@pytest.mark.parametrize("B", [129, 255, 256, 257, 1023, 1024, 1025, 5000, 65536])
 def test_offsets_large_batches(B):
     rng = np.random.default_rng(B)
     L = rng.integers(0, 40, size=B).astype(np.int32)  # many ties
