@@ -67,7 +67,21 @@ struct Cfg {
     static constexpr int kLdsBytes = kStageBytes > kEpilogueBytes ? kStageBytes : kEpilogueBytes;
     static_assert(kLdsBytes <= 160 * 1024, "LDS budget");
     static_assert(kXBlocks >= 1 && kWBlocks >= 1, "copy split");
+    // Paired-w pipeline (BM = 128, w stored [N][K]): two x stages of BK and two w
+    // stages of 2 BK, 80 KB, still two workgroups per CU.
+    static constexpr int kPairXElems = BM * BK, kPairWElems = BN * 2 * BK;
+    static constexpr int kPairWBlocks = BN / 8 / kWaves;  // 1 KB copies of w per wave and w stage
+    static constexpr int kPairBytes = (2 * kPairXElems + 2 * kPairWElems) * 2;
+    static constexpr int kPairLdsBytes = kPairBytes > kEpilogueBytes ? kPairBytes : kEpilogueBytes;
+    static_assert(BM != 128 || 2 * kPairLdsBytes <= 160 * 1024, "two paired-w workgroups per CU");
 };
+
+// The pipeline a tile runs: paired-w for 128-token tiles with w stored [N][K],
+// the kStages ring otherwise (256-token tiles; the [K][N] and triangular
+// operands of trmm).
+constexpr bool pair_w(int bm, bool w_kn, bool tri) { return bm == 128 && !w_kn && !tri; }
+template <int BM, bool W_KN, bool TRI = false>
+constexpr int tile_lds_bytes() { return pair_w(BM, W_KN, TRI) ? Cfg<BM>::kPairLdsBytes : Cfg<BM>::kLdsBytes; }
 
 // The 16-byte chunk index inside an LDS row is XOR-swizzled with bits 2-3 of the
 // row: a ds_read_b128 serves 16 lanes per cycle, here 16 consecutive rows (four
@@ -113,6 +127,18 @@ constexpr int kKnChunks = BN / 8;
 constexpr int kKnRowsPerBlock = 64 / kKnChunks;  // rows one 1 KB wave copy fills
 __device__ __forceinline__ int swz_kn(int row) { return (row & 3) << 2; }
 
+// Paired-w stages: BN rows of 2 BK (128 bytes, eight 16-byte chunks) whose chunk
+// index is XOR-swizzled with bits 1-3 of the row, so the fragment reads of 16
+// consecutive rows (two rows per 256-byte bank line) hit 16 distinct bank groups.
+// A 1 KB wave copy fills 8 whole rows, so every copy request is a full 128-byte
+// line: half as many L2 requests as 64-byte K-step rows.
+__device__ __forceinline__ int swz2(int row) { return (row >> 1) & 7; }
+
+template <int N>
+__device__ __forceinline__ void wait_vm() {
+    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+
 typedef __attribute__((ext_vector_type(4))) short short4_t;
 typedef __attribute__((address_space(3))) short4_t lds_short4_t;
 
@@ -155,7 +181,7 @@ __device__ __forceinline__ void wait_copies(int n) {
 }
 
 // One BM x BN output tile at (m0, n0) of y = act(x w^T + bias) + residual, w being
-// [N, K] with K contiguous; smem holds Cfg<BM>::kLdsBytes.  Called by the workgroup
+// [N, K] with K contiguous; smem holds tile_lds_bytes<BM, W_KN, TRI>().  Called by the workgroup
 // as a whole (it synchronises on LDS).  K (a multiple of 64) is the extent of the
 // reduction the tile runs.
 //   W_KN  w is instead [K rows][N] with leading dimension ldw and kvalid valid
@@ -171,7 +197,9 @@ __device__ __forceinline__ void gemm_tile_bf16(const uint16_t* __restrict__ x, i
                                                uint16_t* smem, int ldw = 0, int kvalid = 0) {
     using C = Cfg<BM>;
     constexpr int kStages = C::kStages, kStageElems = C::kStageElems, kCopies = C::kCopies;
-    const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
+    constexpr bool kPW = pair_w(BM, W_KN, TRI);
+    // wave-uniform by construction; made explicit so that LDS copy addresses stay scalar
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave), lane = threadIdx.x % kWave;
     const int wm = wave / 4, wn = wave % 4;
     const int l32 = lane % 32, h2 = lane / 32;
 
@@ -193,19 +221,24 @@ __device__ __forceinline__ void gemm_tile_bf16(const uint16_t* __restrict__ x, i
             vw[i] = copy_voffset(lane, (wave * C::kWBlocks + i) * kRowsPerBlock, K * 2);
         }
     }
-    auto issue = [&](int step) {
+    // copy c of this wave for `step`: x blocks first, then w blocks
+    auto issue_one = [&](int step, int c) {
         uint16_t* xs = smem + (step % kStages) * kStageElems;
         uint16_t* ws = xs + BM * BK;
         const int k0b = step * BK * 2;
-#pragma unroll
-        for (int i = 0; i < C::kXBlocks; ++i) copy_block(rx, xs + (wave * C::kXBlocks + i) * 512, vx[i], k0b);
-#pragma unroll
-        for (int i = 0; i < C::kWBlocks; ++i) {
+        if (c < C::kXBlocks) {
+            copy_block(rx, xs + (wave * C::kXBlocks + c) * 512, vx[c], k0b);
+        } else {
+            const int i = c - C::kXBlocks;
             if constexpr (W_KN)  // the step moves down the rows: keep it in the range-checked offset
                 copy_block(rw, ws + (wave * C::kWBlocks + i) * 512, vw[i] + step * BK * ldw * 2, 0);
             else
                 copy_block(rw, ws + (wave * C::kWBlocks + i) * 512, vw[i], k0b);
         }
+    };
+    auto issue = [&](int step) {
+#pragma unroll
+        for (int c = 0; c < kCopies; ++c) issue_one(step, c);
     };
     // transposed-read addresses of the [K][N] layout: rows 8 h2 + e (+4), columns
     // wn*WN + i*32 + 16 (g & 1) + 4q, g = lane / 16 (so the lane's column is l32)
@@ -264,7 +297,10 @@ __device__ __forceinline__ void gemm_tile_bf16(const uint16_t* __restrict__ x, i
                          bf16x8 (&nb)[KSTEPS][FM], int kt, int nk, auto masked) {
         wait_copies<kCopies>(min(kStages - 2, nk - 2 - kt) * kCopies);
         barrier_lds();  // step kt+1's stage is visible; step kt's stage is no longer read
-        if (kt + kStages < nk) issue(kt + kStages);
+        // TRI issues the step's copies at once (spread over the MFMAs they push the
+        // edge loop past the register budget); otherwise one MFMA group apart
+        const bool copy = kt + kStages < nk;
+        if (TRI && copy) issue(kt + kStages);
         if constexpr (decltype(masked)::value) mask_x(kt + 1);
         read_x(nb, kt + 1);
 #pragma unroll
@@ -274,6 +310,11 @@ __device__ __forceinline__ void gemm_tile_bf16(const uint16_t* __restrict__ x, i
 #pragma unroll
                 for (int j = 0; j < FM; ++j) acc[i][j] = mfma32x32x16(fa[ks][i], fb[ks][j], acc[i][j]);
                 read_w1(na, kt + 1, ks, i);
+                if (!TRI && copy) {
+#pragma unroll
+                    for (int c = 0; c < kCopies; ++c)
+                        if (c % (KSTEPS * FN) == ks * FN + i) issue_one(kt + kStages, c);
+                }
             }
     };
     auto step_last = [&](bf16x8 (&fa)[KSTEPS][FN], bf16x8 (&fb)[KSTEPS][FM]) {
@@ -286,11 +327,107 @@ __device__ __forceinline__ void gemm_tile_bf16(const uint16_t* __restrict__ x, i
     };
 
     const int nk = K / BK;
+    constexpr std::bool_constant<false> plain{};
+    constexpr std::bool_constant<TRI> edge{};
+    if constexpr (kPW) {
+        // Paired-w pipeline.  x step s lives in x stage s & 1, w steps 2q and 2q + 1 in
+        // w stage q & 1 (one 128-byte row per feature).  Step kt (after its barrier)
+        // copies x of step kt + 2 into the x stage step kt has left, and an odd step
+        // also copies w pair (kt + 3) / 2 into the w stage steps kt - 1 and kt have
+        // left.  Each step's x copies go out first, so the barrier of step kt waits
+        // for x of step kt + 1 with only that step's later w copies still allowed in
+        // flight.
+        const int np = nk / 2;  // K is a multiple of 64
+        constexpr int kXE = C::kPairXElems, kWE = C::kPairWElems, kPWB = C::kPairWBlocks;
+        uint16_t* const xs0 = smem;
+        uint16_t* const ws0 = smem + 2 * kXE;
+        // w copy i of this wave fills rows 8 b .. 8 b + 7, b = wave * kPWB + i, lane l
+        // landing in slot l (row 8 b + l / 8, physical chunk l % 8).  Blocks i and
+        // i + 2 are 16 rows apart and share the swizzle, so two offsets serve all.
+        int vwp[2];
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            const int row = (wave * kPWB + h) * 8 + lane / 8;
+            vwp[h] = row * K * 2 + ((lane % 8) ^ swz2(row)) * 16;
+        }
+        auto issue_x = [&](int step) {
+            uint16_t* xs = xs0 + (step & 1) * kXE;
+#pragma unroll
+            for (int i = 0; i < C::kXBlocks; ++i)
+                copy_block(rx, xs + (wave * C::kXBlocks + i) * 512, vx[i], step * BK * 2);
+        };
+        auto issue_w = [&](int pair, int i) {
+            copy_block(rw, ws0 + (pair & 1) * kWE + (wave * kPWB + i) * 512, vwp[i & 1] + (i >> 1) * 32 * K,
+                       pair * 4 * BK);
+        };
+        auto read_xp = [&](bf16x8 (&fb)[KSTEPS][FM], int step) {
+            const uint16_t* xb = xs0 + (step & 1) * kXE;
+#pragma unroll
+            for (int ks = 0; ks < KSTEPS; ++ks)
+#pragma unroll
+                for (int j = 0; j < FM; ++j) fb[ks][j] = lds_frag(xb, wm * WM + j * 32 + l32, ks * 2 + h2);
+        };
+        // step's parity is a compile-time constant at every call
+        auto read_wp = [&](bf16x8 (&fa)[KSTEPS][FN], int step, int ks, int i, auto odd) {
+            const uint16_t* wb = ws0 + ((step >> 1) & 1) * kWE;
+            const int row = wn * WN + i * 32 + l32;
+            const int chunk = (decltype(odd)::value ? 4 : 0) + ks * 2 + h2;
+            fa[ks][i] = as_bf16x8(*reinterpret_cast<const u32x4*>(wb + row * 2 * BK + ((chunk ^ swz2(row)) * 8)));
+        };
+        constexpr std::bool_constant<false> even{};
+        constexpr std::bool_constant<true> odd{};
+        auto step_pair = [&](bf16x8 (&fa)[KSTEPS][FN], bf16x8 (&fb)[KSTEPS][FM], bf16x8 (&na)[KSTEPS][FN],
+                             bf16x8 (&nb)[KSTEPS][FM], int kt, auto kt_odd) {
+            constexpr bool kOdd = decltype(kt_odd)::value;
+            if constexpr (kOdd) wait_vm<0>();  // x of step kt + 1 was the last copy issued
+            else if ((kt >> 1) + 1 < np) wait_vm<kPWB>();
+            else wait_vm<0>();
+            barrier_lds();  // step kt+1's operands are visible; step kt's x stage is free
+            if (kt + 2 < nk) issue_x(kt + 2);
+            const bool wcopy = kOdd && ((kt + 3) >> 1) < np;
+            read_xp(nb, kt + 1);
+#pragma unroll
+            for (int ks = 0; ks < KSTEPS; ++ks)
+#pragma unroll
+                for (int i = 0; i < FN; ++i) {
+#pragma unroll
+                    for (int j = 0; j < FM; ++j) acc[i][j] = mfma32x32x16(fa[ks][i], fb[ks][j], acc[i][j]);
+                    read_wp(na, kt + 1, ks, i, std::bool_constant<!kOdd>{});
+                    if (wcopy) {  // spread over the step's MFMAs
+#pragma unroll
+                        for (int c = 0; c < kPWB; ++c)
+                            if (c % (KSTEPS * FN) == ks * FN + i) issue_w((kt + 3) >> 1, c);
+                    }
+                }
+        };
+        issue_x(0);
+#pragma unroll
+        for (int c = 0; c < kPWB; ++c) issue_w(0, c);
+        issue_x(1);
+        if (np > 1) {
+#pragma unroll
+            for (int c = 0; c < kPWB; ++c) issue_w(1, c);
+            wait_vm<C::kXBlocks + kPWB>();
+        } else {
+            wait_vm<C::kXBlocks>();
+        }
+        barrier_lds();
+        read_xp(fb0, 0);
+#pragma unroll
+        for (int ks = 0; ks < KSTEPS; ++ks)
+#pragma unroll
+            for (int i = 0; i < FN; ++i) read_wp(fa0, 0, ks, i, even);
+        int kt = 0;
+        for (; kt + 2 < nk; kt += 2) {
+            step_pair(fa0, fb0, fa1, fb1, kt, even);
+            step_pair(fa1, fb1, fa0, fb0, kt + 1, odd);
+        }
+        step_pair(fa0, fb0, fa1, fb1, nk - 2, even);
+        step_last(fa1, fb1);
+    } else {
     // TRI: steps below kfree have every k under the tile's first row (no check);
     // the rest form the separately compiled edge loop
     const int kfree = TRI ? min(m0 / BK, nk) : nk;
-    constexpr std::bool_constant<false> plain{};
-    constexpr std::bool_constant<TRI> edge{};
 #pragma unroll
     for (int st = 0; st < kStages; ++st)
         if (st < nk) issue(st);
@@ -316,6 +453,7 @@ __device__ __forceinline__ void gemm_tile_bf16(const uint16_t* __restrict__ x, i
     }
     step_next(fa0, fb0, fa1, fb1, nk - 2, nk, edge);
     step_last(fa1, fb1);
+    }
 
     // Epilogue through LDS, 32 tokens at a time: the waves holding a slice write
     // their fp32 accumulators there, then all waves read whole rows back (16 bytes
@@ -653,15 +791,16 @@ template <int BM, int ACT, bool HB, bool HR>
 hipError_t launch_bf16_tiles(const void* x, int ldx, const void* w, const void* bias, const void* residual, int ldr,
                              void* y, int ldy, int T, int K, int N, hipStream_t s) {
     using C = Cfg<BM>;
+    constexpr int kLds = tile_lds_bytes<BM, false>();
     const int tiles_m = (T + BM - 1) / BM, tiles_n = (N + BN - 1) / BN;
     static bool attr_set = false;  // benign race: every thread sets the same value
     if (!attr_set) {
         hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_gemm_bf16<BM, ACT, HB, HR>),
-                                           hipFuncAttributeMaxDynamicSharedMemorySize, C::kLdsBytes);
+                                           hipFuncAttributeMaxDynamicSharedMemorySize, kLds);
         if (e != hipSuccess) return e;
         attr_set = true;
     }
-    hipLaunchKernelGGL((k_gemm_bf16<BM, ACT, HB, HR>), dim3(tiles_m * tiles_n), dim3(C::kThreads), C::kLdsBytes, s,
+    hipLaunchKernelGGL((k_gemm_bf16<BM, ACT, HB, HR>), dim3(tiles_m * tiles_n), dim3(C::kThreads), kLds, s,
                        static_cast<const uint16_t*>(x), ldx, static_cast<const uint16_t*>(w),
                        static_cast<const uint16_t*>(bias), static_cast<const uint16_t*>(residual), ldr,
                        static_cast<uint16_t*>(y), ldy, T, K, N, tiles_m, tiles_n);
@@ -701,14 +840,15 @@ hipError_t launch_vgemm(const VgemmView& p, int dtype, const void* a, int64_t a_
     const int64_t grid = (p.tile_cap + kVgemmGridQuantum - 1) / kVgemmGridQuantum * kVgemmGridQuantum;
     if (dtype == 1) {
         using C = Cfg<kVgemmTileM>;
+        constexpr int kLds = tile_lds_bytes<kVgemmTileM, false>();
         static bool attr_set = false;  // benign race: every thread sets the same value
         if (!attr_set) {
             hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_vgemm_bf16),
-                                               hipFuncAttributeMaxDynamicSharedMemorySize, C::kLdsBytes);
+                                               hipFuncAttributeMaxDynamicSharedMemorySize, kLds);
             if (e != hipSuccess) return e;
             attr_set = true;
         }
-        hipLaunchKernelGGL(k_vgemm_bf16, dim3((unsigned)grid), dim3(C::kThreads), C::kLdsBytes, s, va,
+        hipLaunchKernelGGL(k_vgemm_bf16, dim3((unsigned)grid), dim3(C::kThreads), kLds, s, va,
                            static_cast<const uint16_t*>(a), static_cast<const uint16_t*>(b), static_cast<uint16_t*>(c));
     } else {
         hipLaunchKernelGGL(k_vgemm_f32, dim3((unsigned)grid), dim3(256), 0, s, va, static_cast<const float*>(a),
@@ -722,17 +862,18 @@ hipError_t launch_trmm(int dtype, const void* l, int ldl, const void* b, int ldb
     if (n == 0 || m == 0) return hipSuccess;
     if (dtype == 1) {
         using C = Cfg<kTrmmTile>;
+        constexpr int kLds = tile_lds_bytes<kTrmmTile, true, true>();
         const int tiles_m = (n + kTrmmTile - 1) / kTrmmTile, tiles_n = (m + BN - 1) / BN;
         const int q = 8 * max(1, tiles_n / 8);  // the grid covers whole rounds of chunks
         const int per_xcd = (tiles_m * tiles_n + q - 1) / q * q / 8;
         static bool attr_set = false;  // benign race: every thread sets the same value
         if (!attr_set) {
             hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_trmm_bf16),
-                                               hipFuncAttributeMaxDynamicSharedMemorySize, C::kLdsBytes);
+                                               hipFuncAttributeMaxDynamicSharedMemorySize, kLds);
             if (e != hipSuccess) return e;
             attr_set = true;
         }
-        hipLaunchKernelGGL(k_trmm_bf16, dim3(8 * per_xcd), dim3(C::kThreads), C::kLdsBytes, s,
+        hipLaunchKernelGGL(k_trmm_bf16, dim3(8 * per_xcd), dim3(C::kThreads), kLds, s,
                            static_cast<const uint16_t*>(l), ldl, static_cast<const uint16_t*>(b), ldb,
                            static_cast<uint16_t*>(c), ldc, n, m, tiles_m, tiles_n);
     } else {
