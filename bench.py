@@ -37,13 +37,12 @@ STAGES = ["qkv_proj", "qkt", "softmax", "attention", "out_proj", "layernorm1", "
 
 def stage_kernels(T, d, dff):
     """Kernel symbol of each timed stage of the bf16 layer with fused attention, following the
-    library's launch rules: 256-token GEMM tiles for wide plain outputs, 128 otherwise;
-    LayerNorm instantiated for the power of two >= d / 512 16-byte chunks per lane."""
-    bm_qkv = 256 if 3 * d >= 2048 and T >= 2048 else 128
+    library's launch rules: 128-token GEMM tiles; LayerNorm instantiated for the power of
+    two >= d / 512 16-byte chunks per lane."""
     chunks = -(-d // 8 // 64)  # 16-byte chunks per lane, rounded up to a power of two
     ln = f"k_layernorm<true, {1 << max(0, (chunks - 1).bit_length())}>"
     return {
-        "qkv_proj": f"k_gemm_bf16<{bm_qkv}, 0, true, false>",
+        "qkv_proj": "k_gemm_bf16<128, 0, true, false>",
         "attention": "k_attention_bf16<false>",
         "out_proj": "k_gemm_bf16<128, 0, true, true>",
         "ff2": "k_gemm_bf16<128, 0, true, true>",

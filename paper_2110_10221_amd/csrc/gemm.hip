@@ -3,11 +3,12 @@
 // fused loop over the batch and length loops, so they are plain GEMMs with
 // M = T and no padding).
 //
-// bf16: a BM x 256 output tile per workgroup of (BM/128) x 4 waves, each wave a
-// 128 (tokens) x 64 (features) sub-tile of v_mfma_f32_32x32x16_bf16 accumulators
-// (the full-rate bf16 MFMA on gfx950).  BM = 128 needs 72 KB of LDS, so two
+// bf16: a 128 x 256 output tile per workgroup of 4 waves, each wave a 128
+// (tokens) x 64 (features) sub-tile of v_mfma_f32_32x32x16_bf16 accumulators
+// (the full-rate bf16 MFMA on gfx950).  A tile needs at most 80 KB of LDS, so two
 // workgroups share a CU and one's prologue / epilogue overlaps the other's K
-// loop; BM = 256 (8 waves, 128 KB) moves a third fewer operand bytes per FLOP.
+// loop.  (256-token tiles of 8 waves, measured against this design, were no
+// faster on 8192^3 and 8% slower on the QKV projection.)
 //  - Both operands are K-contiguous in memory (x is [T, K], w is [N, K]), the
 //    operand layout the MFMA wants, so tiles go to LDS untransposed.
 //  - Global -> LDS copies are bounds-checked buffer loads that write LDS
@@ -18,11 +19,17 @@
 //  - The 16-byte chunk index inside an LDS row is XOR-swizzled with the row, so
 //    the fragment reads of 16 consecutive rows hit 16 distinct bank groups; the
 //    copies pick their source chunk so that the swizzled slot is filled.
-//  - Software pipeline over K steps of 32: kStages LDS stages, copies issued
-//    kStages steps ahead; the x fragments of step k+1 are read into a second
-//    register set right after the barrier and its w fragments are streamed in
-//    while the MFMAs of step k run.  The barrier waits only for the copies the
-//    next step needs.
+//  - Software pipeline over K steps of 32: the x fragments of step k+1 are read
+//    into a second register set right after the step's barrier and its w
+//    fragments are streamed in while the MFMAs of step k run; the barrier waits
+//    only for the copies the next step needs, and the copies of later steps are
+//    issued one MFMA group apart.  Two LDS layouts:
+//      paired-w (GEMM, vgemm): x in two stages of 32 k, w in two stages of 64 k
+//        (one 128-byte row per feature), 80 KB.  Every w copy reads whole
+//        128-byte lines, which halves the L2 requests of the dominant operand
+//        (64-byte K-step rows cost one request per half line; measured 11-15%
+//        faster on the layer's GEMMs).
+//      ring (trmm): three stages of 32 k, copies issued three steps ahead, 72 KB.
 //  - The MFMA computes the transposed tile C[n][m] = sum_k w[n][k] x[m][k], so each
 //    lane ends with four consecutive output features of one token.  The fp32
 //    results pass through LDS in 32-token slices so that bias / activation /
@@ -52,9 +59,8 @@ constexpr int kRowsPerBlock = 64 / kChunks; // rows filled by one 1 KB wave copy
 constexpr int kEpiRows = 32;                // tokens per epilogue slice
 constexpr int kGroupM = 8;                  // token tiles per group in the tile order
 
-// Tile configurations: BM = 128 (4 waves, 3 stages, 72 KB: two workgroups per CU)
-// and BM = 256 (8 waves, 4 stages, 128 KB: one workgroup of two waves per SIMD,
-// a third fewer operand bytes per FLOP).
+// Tile configuration: BM tokens x BN features per workgroup of BM / 128 x 4 waves
+// (every launch here uses BM = 128: 4 waves, two workgroups per CU).
 template <int BM>
 struct Cfg {
     static constexpr int kWavesM = BM / 128, kWaves = kWavesM * 4, kThreads = kWaves * kWave;
@@ -155,17 +161,14 @@ __device__ __forceinline__ bf16x8 lds_frag_tr(const uint16_t* lo_addr, const uin
 // Output tile of a linear workgroup id.  Workgroups are dealt to the 8 XCDs
 // round-robin, so the id is first remapped to give each XCD a contiguous range.
 // That range is walked in groups of kGroupM token tiles, token tile fastest, so
-// the tiles an XCD runs at once share both x rows and w rows in its L2 -- except
-// for a narrow output with a long K (few feature tiles, x tiles of 1 MB and
-// more), where token-major order lets the workgroups that start together share
-// each x tile (measured faster there).
-__device__ __forceinline__ void tile_coords(int bid, int nblocks, int tiles_m, int tiles_n, int K, int& tm, int& tn) {
+// the tiles an XCD runs at once share both x rows and w rows in its L2 (groups of
+// 2 to 16 measured alike on the layer's GEMMs except FF1, slower below 8).
+__device__ __forceinline__ void tile_coords(int bid, int nblocks, int tiles_m, int tiles_n, int& tm, int& tn) {
     const int per = nblocks / 8, rem = nblocks % 8;
     const int xcd = bid % 8, idx = bid / 8;
     const int t = xcd < rem ? xcd * (per + 1) + idx : rem * (per + 1) + (xcd - rem) * per + idx;
-    const int group = (tiles_n < 8 && K > 2048) ? 1 : kGroupM;
-    const int gsz = group * tiles_n, first = (t / gsz) * group;
-    const int gm = min(tiles_m - first, group);
+    const int gsz = kGroupM * tiles_n, first = (t / gsz) * kGroupM;
+    const int gm = min(tiles_m - first, kGroupM);
     tm = first + (t % gsz) % gm;
     tn = (t % gsz) / gm;
 }
@@ -531,7 +534,7 @@ void k_gemm_bf16(const uint16_t* __restrict__ x, int ldx, const uint16_t* __rest
                  int T, int K, int N, int tiles_m, int tiles_n) {
     extern __shared__ __attribute__((aligned(16))) uint16_t smem[];
     int tm, tn;
-    tile_coords(blockIdx.x, gridDim.x, tiles_m, tiles_n, K, tm, tn);
+    tile_coords(blockIdx.x, gridDim.x, tiles_m, tiles_n, tm, tn);
     gemm_tile_bf16<BM, ACT, HAS_BIAS, HAS_RES>(x, ldx, w, bias, residual, ldr, y, ldy, T, K, N, tm * BM, tn * BN, smem);
 }
 
@@ -807,27 +810,14 @@ hipError_t launch_bf16_tiles(const void* x, int ldx, const void* w, const void* 
     return hipGetLastError();
 }
 
-// 256-token tiles read a third fewer operand bytes per FLOP but run one
-// workgroup per CU, so nothing hides their epilogue and their last round of
-// tiles is coarser: measured on the encoder shapes they pay off for wide
-// outputs (N >= 2048) with a plain epilogue.
-template <int ACT, bool HB, bool HR>
-hipError_t launch_bf16_variant(const void* x, int ldx, const void* w, const void* bias, const void* residual,
-                               int ldr, void* y, int ldy, int T, int K, int N, hipStream_t s) {
-    if constexpr (ACT == 0 && !HR) {
-        if (N >= 2048 && T >= 2048)
-            return launch_bf16_tiles<256, ACT, HB, HR>(x, ldx, w, bias, residual, ldr, y, ldy, T, K, N, s);
-    }
-    return launch_bf16_tiles<128, ACT, HB, HR>(x, ldx, w, bias, residual, ldr, y, ldy, T, K, N, s);
-}
-
 template <int ACT>
 hipError_t launch_bf16_act(const void* x, int ldx, const void* w, const void* bias, const void* residual, int ldr,
                            void* y, int ldy, int T, int K, int N, hipStream_t s) {
-    if (bias && residual) return launch_bf16_variant<ACT, true, true>(x, ldx, w, bias, residual, ldr, y, ldy, T, K, N, s);
-    if (bias) return launch_bf16_variant<ACT, true, false>(x, ldx, w, bias, residual, ldr, y, ldy, T, K, N, s);
-    if (residual) return launch_bf16_variant<ACT, false, true>(x, ldx, w, bias, residual, ldr, y, ldy, T, K, N, s);
-    return launch_bf16_variant<ACT, false, false>(x, ldx, w, bias, residual, ldr, y, ldy, T, K, N, s);
+    auto* f = &launch_bf16_tiles<128, ACT, false, false>;
+    if (bias && residual) f = &launch_bf16_tiles<128, ACT, true, true>;
+    else if (bias) f = &launch_bf16_tiles<128, ACT, true, false>;
+    else if (residual) f = &launch_bf16_tiles<128, ACT, false, true>;
+    return f(x, ldx, w, bias, residual, ldr, y, ldy, T, K, N, s);
 }
 
 }  // namespace
