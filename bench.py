@@ -37,16 +37,17 @@ STAGES = ["qkv_proj", "qkt", "softmax", "attention", "out_proj", "layernorm1", "
 
 def stage_kernels(T, d, dff):
     """Kernel symbol of each timed stage of the bf16 layer with fused attention, following the
-    library's launch rules: 128-token GEMM tiles; LayerNorm instantiated for the power of
-    two >= d / 512 16-byte chunks per lane."""
+    library's launch rules: one GEMM kernel per epilogue (128-token tiles, a sparse last
+    round as 64-token halves); LayerNorm instantiated for the power of two >= d / 512
+    16-byte chunks per lane."""
     chunks = -(-d // 8 // 64)  # 16-byte chunks per lane, rounded up to a power of two
     ln = f"k_layernorm<true, {1 << max(0, (chunks - 1).bit_length())}>"
     return {
-        "qkv_proj": "k_gemm_bf16<128, 0, true, false>",
+        "qkv_proj": "k_gemm_bf16<0, true, false>",
         "attention": "k_attention_bf16<false>",
-        "out_proj": "k_gemm_bf16<128, 0, true, true>",
-        "ff2": "k_gemm_bf16<128, 0, true, true>",
-        "ff1": "k_gemm_bf16<128, 1, true, false>",
+        "out_proj": "k_gemm_bf16<0, true, true>",
+        "ff2": "k_gemm_bf16<0, true, true>",
+        "ff1": "k_gemm_bf16<1, true, false>",
         "layernorm1": ln,
         "layernorm2": ln,
     }

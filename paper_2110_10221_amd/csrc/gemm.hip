@@ -51,20 +51,22 @@ namespace {
 typedef __attribute__((address_space(3))) void lds_void_t;
 
 constexpr int BN = 256, BK = 32;
-constexpr int WM = 128, WN = 64;            // wave tile (tokens x features)
-constexpr int FM = WM / 32, FN = WN / 32;   // 32x32 fragments per wave
+constexpr int WN = 64, FN = WN / 32;        // wave tile: all BM tokens x WN features
 constexpr int KSTEPS = BK / 16;             // MFMA k-steps per K step
 constexpr int kChunks = BK / 8;             // 16-byte chunks per LDS row
 constexpr int kRowsPerBlock = 64 / kChunks; // rows filled by one 1 KB wave copy
 constexpr int kEpiRows = 32;                // tokens per epilogue slice
 constexpr int kGroupM = 8;                  // token tiles per group in the tile order
 
-// Tile configuration: BM tokens x BN features per workgroup of BM / 128 x 4 waves
-// (every launch here uses BM = 128: 4 waves, two workgroups per CU).
+// Tile configuration: BM tokens x BN features per workgroup of 4 waves, wave w
+// holding all BM tokens x features [64 w, 64 w + 64); BM = 128, or 64 for the
+// halves of a last round's tiles.  Two workgroups share a CU.
 template <int BM>
 struct Cfg {
-    static constexpr int kWavesM = BM / 128, kWaves = kWavesM * 4, kThreads = kWaves * kWave;
-    static constexpr int kStages = BM == 128 ? 3 : 4;
+    static_assert(BM == 64 || BM == 128, "tile height");
+    static constexpr int kWaves = 4, kThreads = kWaves * kWave;
+    static constexpr int kFM = BM / 32;                 // 32-token fragments per wave
+    static constexpr int kStages = 3;
     static constexpr int kStageElems = (BM + BN) * BK;  // one LDS stage: x tile then w tile
     static constexpr int kXBlocks = BM / kRowsPerBlock / kWaves;  // 1 KB copies of x per wave and step
     static constexpr int kWBlocks = BN / kRowsPerBlock / kWaves;  // 1 KB copies of w per wave and step
@@ -73,19 +75,18 @@ struct Cfg {
     static constexpr int kLdsBytes = kStageBytes > kEpilogueBytes ? kStageBytes : kEpilogueBytes;
     static_assert(kLdsBytes <= 160 * 1024, "LDS budget");
     static_assert(kXBlocks >= 1 && kWBlocks >= 1, "copy split");
-    // Paired-w pipeline (BM = 128, w stored [N][K]): two x stages of BK and two w
-    // stages of 2 BK, 80 KB, still two workgroups per CU.
+    // Paired-w pipeline (w stored [N][K]): two x stages of BK and two w stages of
+    // 2 BK, at most 80 KB, still two workgroups per CU.
     static constexpr int kPairXElems = BM * BK, kPairWElems = BN * 2 * BK;
     static constexpr int kPairWBlocks = BN / 8 / kWaves;  // 1 KB copies of w per wave and w stage
     static constexpr int kPairBytes = (2 * kPairXElems + 2 * kPairWElems) * 2;
     static constexpr int kPairLdsBytes = kPairBytes > kEpilogueBytes ? kPairBytes : kEpilogueBytes;
-    static_assert(BM != 128 || 2 * kPairLdsBytes <= 160 * 1024, "two paired-w workgroups per CU");
+    static_assert(2 * kPairLdsBytes <= 160 * 1024, "two paired-w workgroups per CU");
 };
 
-// The pipeline a tile runs: paired-w for 128-token tiles with w stored [N][K],
-// the kStages ring otherwise (256-token tiles; the [K][N] and triangular
-// operands of trmm).
-constexpr bool pair_w(int bm, bool w_kn, bool tri) { return bm == 128 && !w_kn && !tri; }
+// The pipeline a tile runs: paired-w with w stored [N][K], the kStages ring
+// otherwise (the [K][N] and triangular operands of trmm).
+constexpr bool pair_w(int, bool w_kn, bool tri) { return !w_kn && !tri; }
 template <int BM, bool W_KN, bool TRI = false>
 constexpr int tile_lds_bytes() { return pair_w(BM, W_KN, TRI) ? Cfg<BM>::kPairLdsBytes : Cfg<BM>::kLdsBytes; }
 
@@ -163,14 +164,18 @@ __device__ __forceinline__ bf16x8 lds_frag_tr(const uint16_t* lo_addr, const uin
 // That range is walked in groups of kGroupM token tiles, token tile fastest, so
 // the tiles an XCD runs at once share both x rows and w rows in its L2 (groups of
 // 2 to 16 measured alike on the layer's GEMMs except FF1, slower below 8).
-__device__ __forceinline__ void tile_coords(int bid, int nblocks, int tiles_m, int tiles_n, int& tm, int& tn) {
-    const int per = nblocks / 8, rem = nblocks % 8;
-    const int xcd = bid % 8, idx = bid / 8;
-    const int t = xcd < rem ? xcd * (per + 1) + idx : rem * (per + 1) + (xcd - rem) * per + idx;
+__device__ __forceinline__ void group_walk(int t, int tiles_m, int tiles_n, int& tm, int& tn) {
     const int gsz = kGroupM * tiles_n, first = (t / gsz) * kGroupM;
     const int gm = min(tiles_m - first, kGroupM);
     tm = first + (t % gsz) % gm;
     tn = (t % gsz) / gm;
+}
+
+__device__ __forceinline__ void tile_coords(int bid, int nblocks, int tiles_m, int tiles_n, int& tm, int& tn) {
+    const int per = nblocks / 8, rem = nblocks % 8;
+    const int xcd = bid % 8, idx = bid / 8;
+    const int t = xcd < rem ? xcd * (per + 1) + idx : rem * (per + 1) + (xcd - rem) * per + idx;
+    group_walk(t, tiles_m, tiles_n, tm, tn);
 }
 
 // Wait until at most `n` copy instructions of this wave are outstanding (the
@@ -201,9 +206,10 @@ __device__ __forceinline__ void gemm_tile_bf16(const uint16_t* __restrict__ x, i
     using C = Cfg<BM>;
     constexpr int kStages = C::kStages, kStageElems = C::kStageElems, kCopies = C::kCopies;
     constexpr bool kPW = pair_w(BM, W_KN, TRI);
+    constexpr int FM = C::kFM;
     // wave-uniform by construction; made explicit so that LDS copy addresses stay scalar
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave), lane = threadIdx.x % kWave;
-    const int wm = wave / 4, wn = wave % 4;
+    const int wn = wave;  // the wave's 64 output features
     const int l32 = lane % 32, h2 = lane / 32;
 
     const __amdgpu_buffer_rsrc_t rx = make_rsrc(x + (int64_t)m0 * ldx, (uint32_t)min(T - m0, BM) * ldx * 2u);
@@ -271,7 +277,7 @@ __device__ __forceinline__ void gemm_tile_bf16(const uint16_t* __restrict__ x, i
 #pragma unroll
         for (int ks = 0; ks < KSTEPS; ++ks)
 #pragma unroll
-            for (int j = 0; j < FM; ++j) fb[ks][j] = lds_frag(xb, wm * WM + j * 32 + l32, ks * 2 + h2);
+            for (int j = 0; j < FM; ++j) fb[ks][j] = lds_frag(xb, j * 32 + l32, ks * 2 + h2);
     };
     // TRI edge steps: zero the x entries with k > i of a landed stage in LDS, then
     // a barrier (the stage is read only after it).  In registers the masks would
@@ -368,7 +374,7 @@ __device__ __forceinline__ void gemm_tile_bf16(const uint16_t* __restrict__ x, i
 #pragma unroll
             for (int ks = 0; ks < KSTEPS; ++ks)
 #pragma unroll
-                for (int j = 0; j < FM; ++j) fb[ks][j] = lds_frag(xb, wm * WM + j * 32 + l32, ks * 2 + h2);
+                for (int j = 0; j < FM; ++j) fb[ks][j] = lds_frag(xb, j * 32 + l32, ks * 2 + h2);
         };
         // step's parity is a compile-time constant at every call
         auto read_wp = [&](bf16x8 (&fa)[KSTEPS][FN], int step, int ks, int i, auto odd) {
@@ -492,17 +498,16 @@ __device__ __forceinline__ void gemm_tile_bf16(const uint16_t* __restrict__ x, i
 #pragma unroll
     for (int slice = 0; slice < BM / kEpiRows; ++slice) {
         barrier_lds();  // the K loop (first slice) or the previous slice is done with LDS
-        if (wm == slice / FM) {
+        // every wave holds the slice's 32 tokens (fragment column `slice`) for its 64 features
 #pragma unroll
-            for (int i = 0; i < FN; ++i)
+        for (int i = 0; i < FN; ++i)
 #pragma unroll
-                for (int g = 0; g < 4; ++g) {
-                    const int c = (wn * WN + i * 32 + 8 * g + 4 * h2) >> 2;
-                    const floatx16& a = acc[i][slice % FM];
-                    const floatx4 o = {a[4 * g], a[4 * g + 1], a[4 * g + 2], a[4 * g + 3]};
-                    *reinterpret_cast<floatx4*>(ep + (l32 * 64 + (c ^ l32)) * 4) = o;
-                }
-        }
+            for (int g = 0; g < 4; ++g) {
+                const int c = (wn * WN + i * 32 + 8 * g + 4 * h2) >> 2;
+                const floatx16& a = acc[i][slice];
+                const floatx4 o = {a[4 * g], a[4 * g + 1], a[4 * g + 2], a[4 * g + 3]};
+                *reinterpret_cast<floatx4*>(ep + (l32 * 64 + (c ^ l32)) * 4) = o;
+            }
         barrier_lds();
 #pragma unroll
         for (int rr = 0; rr < kRowsPerWave; ++rr) {
@@ -527,15 +532,29 @@ __device__ __forceinline__ void gemm_tile_bf16(const uint16_t* __restrict__ x, i
     }
 }
 
-template <int BM, int ACT, bool HAS_BIAS, bool HAS_RES>
-__global__ __launch_bounds__(Cfg<BM>::kThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
+// Packed linear: workgroups [0, n_full) run 128-token tiles in the grouped
+// XCD-aware order; when the last round of tiles would fill at most half the
+// workgroup slots (two per CU), its tiles instead run as two 64-token halves
+// each, workgroups n_full onwards, so that round takes about half a tile's time.
+template <int ACT, bool HAS_BIAS, bool HAS_RES>
+__global__ __launch_bounds__(Cfg<128>::kThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void k_gemm_bf16(const uint16_t* __restrict__ x, int ldx, const uint16_t* __restrict__ w,
                  const uint16_t* __restrict__ bias, const uint16_t* residual, int ldr, uint16_t* y, int ldy,
-                 int T, int K, int N, int tiles_m, int tiles_n) {
+                 int T, int K, int N, int tiles_m, int tiles_n, int n_full) {
     extern __shared__ __attribute__((aligned(16))) uint16_t smem[];
     int tm, tn;
-    tile_coords(blockIdx.x, gridDim.x, tiles_m, tiles_n, tm, tn);
-    gemm_tile_bf16<BM, ACT, HAS_BIAS, HAS_RES>(x, ldx, w, bias, residual, ldr, y, ldy, T, K, N, tm * BM, tn * BN, smem);
+    if ((int)blockIdx.x < n_full) {
+        tile_coords(blockIdx.x, n_full, tiles_m, tiles_n, tm, tn);
+        gemm_tile_bf16<128, ACT, HAS_BIAS, HAS_RES>(x, ldx, w, bias, residual, ldr, y, ldy, T, K, N, tm * 128,
+                                                    tn * BN, smem);
+    } else {
+        const int u = blockIdx.x - n_full;
+        group_walk(n_full + (u >> 1), tiles_m, tiles_n, tm, tn);
+        const int m0 = tm * 128 + (u & 1) * 64;
+        if (m0 >= T) return;  // the lower half of a tile past the last token
+        gemm_tile_bf16<64, ACT, HAS_BIAS, HAS_RES>(x, ldx, w, bias, residual, ldr, y, ldy, T, K, N, m0, tn * BN,
+                                                   smem);
+    }
 }
 
 // fp32: 64x64 tiles, K step 16, 4x4 outputs per thread, plain FMA.
@@ -790,33 +809,36 @@ __global__ __launch_bounds__(256) void k_trmm_f32(const float* __restrict__ l, i
     }
 }
 
-template <int BM, int ACT, bool HB, bool HR>
+template <int ACT, bool HB, bool HR>
 hipError_t launch_bf16_tiles(const void* x, int ldx, const void* w, const void* bias, const void* residual, int ldr,
                              void* y, int ldy, int T, int K, int N, hipStream_t s) {
-    using C = Cfg<BM>;
-    constexpr int kLds = tile_lds_bytes<BM, false>();
-    const int tiles_m = (T + BM - 1) / BM, tiles_n = (N + BN - 1) / BN;
+    constexpr int kLds = tile_lds_bytes<128, false>() > tile_lds_bytes<64, false>() ? tile_lds_bytes<128, false>()
+                                                                                    : tile_lds_bytes<64, false>();
+    const int tiles_m = (T + 127) / 128, tiles_n = (N + BN - 1) / BN, tiles = tiles_m * tiles_n;
+    const int slots = 2 * device_cu_count();                      // resident workgroups
+    const int last = tiles - (tiles - 1) / slots * slots;         // tiles in the last round, 1..slots
+    const int n_full = 2 * last <= slots ? tiles - last : tiles;  // the rest run as halves
     static bool attr_set = false;  // benign race: every thread sets the same value
     if (!attr_set) {
-        hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_gemm_bf16<BM, ACT, HB, HR>),
+        hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_gemm_bf16<ACT, HB, HR>),
                                            hipFuncAttributeMaxDynamicSharedMemorySize, kLds);
         if (e != hipSuccess) return e;
         attr_set = true;
     }
-    hipLaunchKernelGGL((k_gemm_bf16<BM, ACT, HB, HR>), dim3(tiles_m * tiles_n), dim3(C::kThreads), kLds, s,
-                       static_cast<const uint16_t*>(x), ldx, static_cast<const uint16_t*>(w),
+    hipLaunchKernelGGL((k_gemm_bf16<ACT, HB, HR>), dim3(n_full + 2 * (tiles - n_full)), dim3(Cfg<128>::kThreads),
+                       kLds, s, static_cast<const uint16_t*>(x), ldx, static_cast<const uint16_t*>(w),
                        static_cast<const uint16_t*>(bias), static_cast<const uint16_t*>(residual), ldr,
-                       static_cast<uint16_t*>(y), ldy, T, K, N, tiles_m, tiles_n);
+                       static_cast<uint16_t*>(y), ldy, T, K, N, tiles_m, tiles_n, n_full);
     return hipGetLastError();
 }
 
 template <int ACT>
 hipError_t launch_bf16_act(const void* x, int ldx, const void* w, const void* bias, const void* residual, int ldr,
                            void* y, int ldy, int T, int K, int N, hipStream_t s) {
-    auto* f = &launch_bf16_tiles<128, ACT, false, false>;
-    if (bias && residual) f = &launch_bf16_tiles<128, ACT, true, true>;
-    else if (bias) f = &launch_bf16_tiles<128, ACT, true, false>;
-    else if (residual) f = &launch_bf16_tiles<128, ACT, false, true>;
+    auto* f = &launch_bf16_tiles<ACT, false, false>;
+    if (bias && residual) f = &launch_bf16_tiles<ACT, true, true>;
+    else if (bias) f = &launch_bf16_tiles<ACT, true, false>;
+    else if (residual) f = &launch_bf16_tiles<ACT, false, true>;
     return f(x, ldx, w, bias, residual, ldr, y, ldy, T, K, N, s);
 }
 
