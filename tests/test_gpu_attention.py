@@ -184,6 +184,32 @@ def _fused_close(got_bits, L, H, q, k, v, scale):
         assert err.mean() <= 4e-3 * mag.mean(), (err.mean(), mag.mean())
 
 
+# every count of 32-query blocks per sequence, 1..16 (lengths 1, 33, ..., 481, 512),
+# with zero lengths between
+BLOCKS_L = [1, 33, 0, 65, 97, 129, 161, 193, 225, 257, 289, 321, 353, 385, 417, 449, 481, 512, 32, 0, 96, 7]
+
+
+@pytest.mark.parametrize("H", [16, 3])
+def test_fused_attention_every_block_count(H):
+    rng = np.random.default_rng(H)
+    L = np.array(BLOCKS_L, np.int32)
+    T = int(L.sum())
+    print(f"fused block counts H={H}", flush=True)
+    q, k, v = (random_storage(rng, (T, H * 64), "bf16", 1.0) for _ in range(3))
+    _fused_close(_fused(L, H, q, k, v, 0.125), L, H, q, k, v, 0.125)
+
+
+def test_fused_attention_large_batch():
+    # 1100 short sequences and two long ones: 2200 (sequence, head) pairs walked by the persistent grid
+    rng = np.random.default_rng(1100)
+    L = rng.integers(0, 41, size=1100).astype(np.int32)
+    L[[3, 700]] = [300, 512]
+    H, T = 2, int(L.sum())
+    print(f"fused B=1100 T={T}", flush=True)
+    q, k, v = (random_storage(rng, (T, H * 64), "bf16", 1.0) for _ in range(3))
+    _fused_close(_fused(L, H, q, k, v, 0.125), L, H, q, k, v, 0.125)
+
+
 def test_fused_attention_sdpa_workload():
     # bf16 ragged attention, batch 32, 8 heads, lengths uniform in [16, 512]
     wl = make_workload(2, seed=0)

@@ -134,6 +134,29 @@ def test_fused_causal_attention(L, H, qk_scale):
     _fused_causal_close(_fused_causal(L, H, q, k, v, 1 / 8), L, H, q, k, v, 1 / 8)
 
 
+@pytest.mark.parametrize("H", [16, 3])
+def test_fused_causal_every_block_count(H):
+    # every count of 32-query blocks per sequence (see the unmasked test) and zero lengths
+    from tests.test_gpu_attention import BLOCKS_L
+
+    rng = np.random.default_rng(100 + H)
+    L = np.array(BLOCKS_L, np.int32)
+    T = int(L.sum())
+    print(f"fused causal block counts H={H}", flush=True)
+    q, k, v = (random_storage(rng, (T, H * 64), "bf16", 1.0) for _ in range(3))
+    _fused_causal_close(_fused_causal(L, H, q, k, v, 0.125), L, H, q, k, v, 0.125)
+
+
+def test_fused_causal_large_batch():
+    rng = np.random.default_rng(1101)
+    L = rng.integers(0, 41, size=1100).astype(np.int32)
+    L[[3, 700]] = [300, 512]
+    H, T = 2, int(L.sum())
+    print(f"fused causal B=1100 T={T}", flush=True)
+    q, k, v = (random_storage(rng, (T, H * 64), "bf16", 1.0) for _ in range(3))
+    _fused_causal_close(_fused_causal(L, H, q, k, v, 0.125), L, H, q, k, v, 0.125)
+
+
 def test_fused_causal_first_rows_and_prefix():
     # each sequence's first output row is V's first row (up to bf16 rounding of an exact copy),
     # and truncating every sequence to its first m tokens leaves rows < m unchanged
