@@ -320,6 +320,106 @@ def sdpa_measurement(rag, cid, seed=0, iters=30):
                         "qkt": "k_qkt_bf16", "softmax": "k_softmax<true>", "attn_v": "k_attn_v_bf16"}}
 
 
+def other_configs_measurement(rag, iters=30):
+    """The other four configurations of the workload table, each on its own path:
+    1 (fp32, operator-level SDPA: prelude + ragged_qkt + ragged_softmax +
+    ragged_attn_v), 2 (bf16 SDPA: the fused kernel, and the operator chain), 3 and 5
+    (bf16 encoder layers, prelude included per layer).  Useful FLOPs count real
+    tokens only; the padded fraction compares them with every sequence padded to
+    the batch's longest."""
+    import torch
+
+    from tests.helpers import dev
+    from workloads import BIAS_NAMES, CONFIGS, LN_NAMES, WEIGHT_NAMES, make_workload
+
+    out = {}
+    for cid in (1, 2, 3, 5):
+        cfg = CONFIGS[cid]
+        wl = make_workload(cid, seed=0)
+        L = wl.lengths.astype(np.float64)
+        T, d, H, dff = wl.total_tokens, cfg.d_model, cfg.heads, cfg.d_ff
+        s2 = float((L * L).sum())
+        plan = rag.Plan(torch.from_numpy(wl.lengths).cuda(), T, cfg.max_len, H)
+        rec = {"workload": f"config {cid}: batch {cfg.batch}, lengths {cfg.lengths}, {H} heads x 64"
+                           + (f", FFN {dff}" if dff else "") + f", {cfg.dtype}, T = {T}"}
+        if cfg.kind == "sdpa":
+            q, k, v = (dev(wl.tensors[n], cfg.dtype).view(T, d) for n in ("q", "k", "v"))
+            tdt = torch.float32 if cfg.dtype == "f32" else torch.bfloat16
+            S = torch.empty(int(H * s2), dtype=tdt, device="cuda")
+            O = torch.empty(T, d, dtype=tdt, device="cuda")
+
+            def chain():
+                rag.ragged_offsets(plan)
+                rag.ragged_qkt(plan, q, k, S, 0.125)
+                rag.ragged_softmax(plan, S)
+                rag.ragged_attn_v(plan, S, v, O)
+
+            fl = 4.0 * d * s2
+            ms = _timed(chain, iters)
+            rec.update({"operator_chain_ms": round(ms, 4),
+                        "operator_chain_useful_tflops": round(fl / (ms * 1e-3) / 1e12, 2)})
+            if cfg.dtype == "bf16":
+                rag.ragged_offsets(plan)
+                ms_f = _timed(lambda: rag.ragged_attention(plan, q, k, v, O, 0.125), iters)
+                rec.update({"fused_attention_ms": round(ms_f, 4),
+                            "fused_attention_useful_tflops": round(fl / (ms_f * 1e-3) / 1e12, 2)})
+            rec["padded_fraction"] = round(1.0 - s2 / (len(L) * float(L.max()) ** 2), 4)
+        else:
+            x = dev(wl.tensors["x"], "bf16")
+            wd = {n: dev(wl.tensors[n], "bf16") for n in WEIGHT_NAMES + BIAS_NAMES + LN_NAMES}
+            wstruct = rag.layer_weights(wd)
+            ws = torch.empty(rag.encoder_layer_workspace(T, cfg.max_len, d, H, dff, rag.RAG_BF16, 0),
+                             dtype=torch.uint8, device="cuda")
+            y = torch.empty(T, d, dtype=torch.bfloat16, device="cuda")
+
+            def layer():
+                rag.ragged_offsets(plan)
+                rag.encoder_layer(plan, x, y, wstruct, dff, ws)
+
+            ms = _timed(layer, iters)
+            ms_pre = _timed(lambda: rag.ragged_offsets(plan), iters)
+            uf = useful_flops(L, d, dff)
+            rec.update({"ms_per_layer": round(ms, 4),
+                        "ms_per_layer_prelude_amortised_6_layers": round(ms - ms_pre * 5 / 6, 4),
+                        "useful_tflops": round(uf / (ms * 1e-3) / 1e12, 1),
+                        "frac_of_bf16_peak": round(uf / (ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
+                        "padded_fraction": round(padded_fraction(L, d, dff), 4)})
+        assert not plan.data_errors(), plan.data_errors()
+        out[f"config{cid}"] = rec
+    return out
+
+
+def measured_peaks(rag, iters=20):
+    """What this GPU sustains next to its published peaks: HBM as torch's 1 GiB
+    device-to-device copy (bytes read + written per second; a lower bound on the
+    sustainable rate, the LayerNorm kernel reaches 6.5 TB/s), and bf16 matrix
+    throughput of hipBLASLt (through torch.mm) and of this library's packed_linear
+    on an 8192^3 product."""
+    import torch
+
+    n = (1 << 30) // 4
+    src = torch.ones(n, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    ms_copy = _timed(lambda: dst.copy_(src), iters)
+    gbs = 2.0 * n * 4 / (ms_copy * 1e-3) / 1e9
+    del src, dst
+    m = 8192
+    g = torch.Generator(device="cuda").manual_seed(3)
+    a = torch.randn(m, m, device="cuda", generator=g).bfloat16()
+    b = torch.randn(m, m, device="cuda", generator=g).bfloat16()
+    c = torch.empty(m, m, device="cuda", dtype=torch.bfloat16)
+    fl = 2.0 * m ** 3
+    # y = a b^T, the layout of a linear layer (a 2-D product: hipBLASLt's fastest form
+    # here, ~1.65 PFLOP/s, against ~1.25 with a contiguous [K, N] operand)
+    ms_blas = _timed(lambda: torch.mm(a, b.t(), out=c), iters)
+    ms_ours = _timed(lambda: rag.packed_linear(a, b, c), iters)
+    return {"hbm_torch_copy_GB_per_s": round(gbs, 1), "hbm_torch_copy_frac_of_peak": round(gbs / PEAK_HBM_GBS, 4),
+            "bf16_gemm_8192_hipblaslt_tflops": round(fl / (ms_blas * 1e-3) / 1e12, 1),
+            "bf16_gemm_8192_packed_linear_tflops": round(fl / (ms_ours * 1e-3) / 1e12, 1),
+            "note": "the roofline fractions in this line are against the published peaks "
+                    f"({PEAK_HBM_GBS:.0f} GB/s, {PEAK_BF16_TFLOPS:.0f} TFLOP/s bf16)"}
+
+
 def vgemm_measurement(rag, batch=128, iters=20):
     """Variable-sized batched GEMM (the paper's matrix-multiplication experiment):
     `batch` problems with m, n, k uniform over the multiples of 128 in [512, 1408],
@@ -417,6 +517,8 @@ def main():
     ap.add_argument("--no-vgemm", action="store_true", help="skip the variable-sized batched GEMM measurement")
     ap.add_argument("--no-trmm", action="store_true", help="skip the triangular matrix multiplication measurement")
     ap.add_argument("--no-sdpa", action="store_true", help="skip the unfused attention operator measurements")
+    ap.add_argument("--no-configs", action="store_true", help="skip configurations 1, 2, 3 and 5")
+    ap.add_argument("--no-peaks", action="store_true", help="skip the measured HBM copy and 8192^3 GEMM rates")
     ap.add_argument("--cpu-target-flops", type=float, default=2.0e10)
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of MIB MiB five times (counter calibration) and exit")
@@ -577,6 +679,10 @@ def main():
         out["vgemm"] = vgemm_measurement(rag)
     if not args.no_trmm:
         out["trmm"] = trmm_measurement(rag)
+    if not args.no_configs:
+        out["other_configs"] = other_configs_measurement(rag)
+    if not args.no_peaks:
+        out["measured_peaks"] = measured_peaks(rag)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(wl, args.cpu_target_flops)
     else:
