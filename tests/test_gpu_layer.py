@@ -87,8 +87,10 @@ def test_benchmark_configs_sampled_sequences(cid, flags):
     got = _gpu_layer(wl.lengths, wl.tensors["x"], w, cfg.d_model, cfg.heads, cfg.d_ff, "bf16", flags)
     L = wl.lengths
     order = np.argsort(-L, kind="stable")
-    # the longest, the shortest and two in between
-    picks = sorted({int(order[0]), int(order[-1]), int(order[len(L) // 2]), int(order[len(L) // 3])})
+    # the longest, the shortest and two in between, and the last in caller order
+    # (its tokens fall in the GEMMs' last tile rows, where a sparse last round of
+    # tiles runs as 64-token halves)
+    picks = sorted({int(order[0]), int(order[-1]), int(order[len(L) // 2]), int(order[len(L) // 3]), len(L) - 1})
     _sample_check(wl, got, picks)
 
 
