@@ -86,9 +86,9 @@ struct Cfg {
 
 // The pipeline a tile runs: paired-w with w stored [N][K], the kStages ring
 // otherwise (the [K][N] and triangular operands of trmm).
-constexpr bool pair_w(int, bool w_kn, bool tri) { return !w_kn && !tri; }
+constexpr bool pair_w(bool w_kn, bool tri) { return !w_kn && !tri; }
 template <int BM, bool W_KN, bool TRI = false>
-constexpr int tile_lds_bytes() { return pair_w(BM, W_KN, TRI) ? Cfg<BM>::kPairLdsBytes : Cfg<BM>::kLdsBytes; }
+constexpr int tile_lds_bytes() { return pair_w(W_KN, TRI) ? Cfg<BM>::kPairLdsBytes : Cfg<BM>::kLdsBytes; }
 
 // The 16-byte chunk index inside an LDS row is XOR-swizzled with bits 2-3 of the
 // row: a ds_read_b128 serves 16 lanes per cycle, here 16 consecutive rows (four
@@ -205,7 +205,7 @@ __device__ __forceinline__ void gemm_tile_bf16(const uint16_t* __restrict__ x, i
                                                uint16_t* smem, int ldw = 0, int kvalid = 0) {
     using C = Cfg<BM>;
     constexpr int kStages = C::kStages, kStageElems = C::kStageElems, kCopies = C::kCopies;
-    constexpr bool kPW = pair_w(BM, W_KN, TRI);
+    constexpr bool kPW = pair_w(W_KN, TRI);
     constexpr int FM = C::kFM;
     // wave-uniform by construction; made explicit so that LDS copy addresses stay scalar
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave), lane = threadIdx.x % kWave;

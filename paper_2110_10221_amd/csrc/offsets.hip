@@ -48,7 +48,8 @@ __device__ __forceinline__ void block_exclusive_scan2(int64_t a, int64_t b, int6
     int64_t pa = 0, pb = 0;
     ta = 0;
     tb = 0;
-    for (int w = 0; w < kScanWaves; ++w) {
+    const int nw = blockDim.x / kWave;  // the launch may use fewer than kScanThreads threads
+    for (int w = 0; w < nw; ++w) {
         if (w < wid) {
             pa += sh_a[w];
             pb += sh_b[w];
@@ -179,7 +180,8 @@ __global__ __launch_bounds__(kScanThreads) void k_plan_small(const int32_t* __re
                                                               int32_t* __restrict__ av_item_off,
                                                               int32_t* __restrict__ status) {
     __shared__ int64_t sh_a[kScanWaves], sh_b[kScanWaves];
-    __shared__ int32_t sL[kScanThreads], sOrder[kScanThreads];
+    __shared__ __attribute__((aligned(16))) int32_t sL[kScanThreads];
+    __shared__ int32_t sOrder[kScanThreads];
     __shared__ int sh_flags, sh_max;
     const int b = threadIdx.x;
     if (b == 0) {
@@ -187,7 +189,7 @@ __global__ __launch_bounds__(kScanThreads) void k_plan_small(const int32_t* __re
         sh_max = 0;
     }
     const int L = b < B ? lengths[b] : 0;
-    sL[b] = L;
+    sL[b] = b < B ? L : -1;  // padding never outranks a length (negative lengths are flagged anyway)
     int flags = 0;
     if (b < B) {
         if (L < 0) flags |= kDataNegLength;
@@ -207,9 +209,14 @@ __global__ __launch_bounds__(kScanThreads) void k_plan_small(const int32_t* __re
     // longest-first rank (a strict total order: every slot written once)
     if (b < B) {
         int rank = 0;
-        for (int k = 0; k < B; ++k) {
-            const int Lk = sL[k];
-            rank += (Lk > L) | ((Lk == L) & (k < b));
+        // four lengths per LDS read, so the reads pipeline instead of each waiting in turn
+#pragma unroll 2
+        for (int k = 0; k < B; k += 4) {
+            const int4 l4 = *reinterpret_cast<const int4*>(sL + k);
+            rank += (l4.x > L) | ((l4.x == L) & (k < b));
+            rank += (l4.y > L) | ((l4.y == L) & (k + 1 < b));
+            rank += (l4.z > L) | ((l4.z == L) & (k + 2 < b));
+            rank += (l4.w > L) | ((l4.w == L) & (k + 3 < b));
         }
         sOrder[rank] = b;
         order[rank] = b;
@@ -418,7 +425,8 @@ hipError_t launch_vgemm_offsets(const VgemmView& p, hipStream_t s) {
 
 hipError_t launch_offsets(const PlanView& p, hipStream_t s) {
     if (p.batch <= kScanThreads) {
-        hipLaunchKernelGGL(k_plan_small, dim3(1), dim3(kScanThreads), 0, s, p.lengths, p.batch, p.total_tokens,
+        const int threads = (p.batch + kWave - 1) / kWave * kWave;  // one thread per sequence
+        hipLaunchKernelGGL(k_plan_small, dim3(1), dim3(threads), 0, s, p.lengths, p.batch, p.total_tokens,
                            p.max_len, p.heads, p.qkt_cap, p.av_cap, p.tok_off, p.att_off, p.order, p.qkt_item_off,
                            p.av_item_off, p.status);
         hipLaunchKernelGGL(k_plan_fill, dim3(p.batch), dim3(256), 0, s, p.lengths, p.order, p.tok_off, p.heads,
