@@ -308,7 +308,7 @@ __global__ __launch_bounds__(kScanThreads) void k_vgemm_scan(const int32_t* __re
     __syncthreads();
     int flags = 0, shape = 0;
     int64_t carry_a = 0, carry_b = 0, carry_c = 0;
-    for (int base = 0; base < B; base += kScanThreads) {
+    for (int base = 0; base < B; base += blockDim.x) {
         const int p = base + threadIdx.x;
         int64_t m = 0, n = 0, k = 0;
         if (p < B) {
@@ -378,7 +378,7 @@ __global__ __launch_bounds__(kScanThreads) void k_vgemm_tile_scan(const int32_t*
                                                                    int32_t* __restrict__ status) {
     __shared__ int64_t sh_a[kScanWaves], sh_b[kScanWaves];
     int64_t carry = 0;
-    for (int base = 0; base < B; base += kScanThreads) {
+    for (int base = 0; base < B; base += blockDim.x) {
         const int r = base + threadIdx.x;
         const int64_t nt = r < B ? vgemm_tiles(dims, order[r]) : 0;
         int64_t e, unused, t, tu;
@@ -413,10 +413,12 @@ __global__ __launch_bounds__(256) void k_vgemm_fill(const int32_t* __restrict__ 
 }  // namespace
 
 hipError_t launch_vgemm_offsets(const VgemmView& p, hipStream_t s) {
-    hipLaunchKernelGGL(k_vgemm_scan, dim3(1), dim3(kScanThreads), 0, s, p.dims, p.batch, p.a_off, p.b_off, p.c_off,
+    // one thread per problem up to kScanThreads (a smaller workgroup synchronises faster)
+    const int threads = std::min(kScanThreads, (p.batch + kWave - 1) / kWave * kWave);
+    hipLaunchKernelGGL(k_vgemm_scan, dim3(1), dim3(threads), 0, s, p.dims, p.batch, p.a_off, p.b_off, p.c_off,
                        p.status);
     hipLaunchKernelGGL(k_vgemm_rank, dim3((p.batch + 255) / 256), dim3(256), 0, s, p.dims, p.batch, p.order);
-    hipLaunchKernelGGL(k_vgemm_tile_scan, dim3(1), dim3(kScanThreads), 0, s, p.dims, p.order, p.batch, p.tile_cap,
+    hipLaunchKernelGGL(k_vgemm_tile_scan, dim3(1), dim3(threads), 0, s, p.dims, p.order, p.batch, p.tile_cap,
                        p.tile_off, p.status);
     hipLaunchKernelGGL(k_vgemm_fill, dim3(p.batch), dim3(256), 0, s, p.dims, p.order, p.tile_off, p.tile_items,
                        p.status);
