@@ -189,9 +189,12 @@ def _short(name):
     return base.split("(")[0].strip()
 
 
-def derive_traffic(fetch_csv, write_csv, cal_fetch_csv, cal_write_csv, copy_mib):
+def derive_traffic(fetch_csv, write_csv, cal_fetch_csv, cal_write_csv, copy_mib, kernels=None):
     """HBM bytes per launch of every library kernel: FETCH_SIZE + WRITE_SIZE (KiB per
-    dispatch), each scaled by copy_bytes / counter for a plain copy of known size."""
+    dispatch), each scaled by copy_bytes / counter for a plain copy of known size.
+    With `kernels` (base names, no template arguments), only those entries are replaced in the existing
+    file, so each kernel's figure can come from a run in which all its dispatches
+    have the shape the bench line reports."""
     fetch, write = _counter_per_dispatch(fetch_csv, "FETCH_SIZE"), _counter_per_dispatch(write_csv, "WRITE_SIZE")
     cf, cw = _counter_per_dispatch(cal_fetch_csv, "FETCH_SIZE"), _counter_per_dispatch(cal_write_csv, "WRITE_SIZE")
     big = lambda d: max(d.values())  # the copy kernel is the dispatch with the largest counts
@@ -199,14 +202,16 @@ def derive_traffic(fetch_csv, write_csv, cal_fetch_csv, cal_write_csv, copy_mib)
     sf, sw = copy_kib / big(cf), copy_kib / big(cw)
     out = {"_calibration": {"copy_mib": copy_mib, "fetch_scale": sf, "write_scale": sw,
                             "copy_fetch_kib": big(cf), "copy_write_kib": big(cw)}}
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    if kernels is not None and os.path.exists(path):
+        out = {**json.load(open(path)), **out}
     for k in fetch:
         short = _short(k)
         src = KERNEL_SOURCES.get(short.split("<")[0])
-        if src is None:
+        if src is None or (kernels is not None and short.split("<")[0] not in kernels):
             continue
         out[short] = {"bytes_per_launch": round((fetch[k] * sf + write.get(k, 0.0) * sw) * 1024.0),
                       "fetch_kib_raw": fetch[k], "write_kib_raw": write.get(k), "source_sha": source_hash(src)}
-    path = os.path.join(ROOT, "profiles", "traffic.json")
     with open(path, "w") as f:
         json.dump(out, f, indent=1, sort_keys=True)
     print(json.dumps(out, indent=1, sort_keys=True))
@@ -519,6 +524,9 @@ def main():
     ap.add_argument("--no-sdpa", action="store_true", help="skip the unfused attention operator measurements")
     ap.add_argument("--no-configs", action="store_true", help="skip configurations 1, 2, 3 and 5")
     ap.add_argument("--no-peaks", action="store_true", help="skip the measured HBM copy and 8192^3 GEMM rates")
+    ap.add_argument("--layer-only", action="store_true",
+                    help="time the layer steps only (no auxiliary measurements, no CPU baseline), so that a "
+                         "profile of the run sees every dispatch of the layer's kernels at the layer's shape")
     ap.add_argument("--cpu-target-flops", type=float, default=2.0e10)
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of MIB MiB five times (counter calibration) and exit")
@@ -526,9 +534,15 @@ def main():
                     help="turn rocprofv3 --pmc FETCH_SIZE / WRITE_SIZE counter files of a bench run and of a "
                          "copy-calibration run into profiles/traffic.json, then exit")
     ap.add_argument("--copy-mib", type=int, default=512, help="size of the calibration copy (for --derive-traffic)")
+    ap.add_argument("--traffic-kernels", default=None,
+                    help="comma-separated kernel base names (e.g. k_vgemm_bf16): --derive-traffic replaces only their entries")
     args = ap.parse_args()
+    if args.layer_only:
+        args.no_masked = args.no_sdpa = args.no_vgemm = args.no_trmm = True
+        args.no_configs = args.no_peaks = args.no_cpu_baseline = True
     if args.derive_traffic:
-        derive_traffic(*args.derive_traffic, copy_mib=args.copy_mib)
+        kernels = set(args.traffic_kernels.split(",")) if args.traffic_kernels else None
+        derive_traffic(*args.derive_traffic, copy_mib=args.copy_mib, kernels=kernels)
         return
     if args.copy_calibration:
         import torch
