@@ -57,7 +57,17 @@ KERNEL_SOURCES = {
     "k_layernorm": "paper_2110_10221_amd/csrc/layernorm.hip",
     "k_vgemm_bf16": "paper_2110_10221_amd/csrc/gemm.hip",
     "k_trmm_bf16": "paper_2110_10221_amd/csrc/gemm.hip",
+    "k_qkt_bf16": "paper_2110_10221_amd/csrc/attention.hip",
+    "k_softmax": "paper_2110_10221_amd/csrc/attention.hip",
+    "k_attn_v_bf16": "paper_2110_10221_amd/csrc/attention.hip",
+    "k_plan_small": "paper_2110_10221_amd/csrc/offsets.hip",
+    "k_plan_fill": "paper_2110_10221_amd/csrc/offsets.hip",
 }
+# unfused operator measurements: kernels of each operator, and the tag under which
+# their counters are stored per workload (the same symbols run at both shapes)
+SDPA_TAGS = {2: "sdpa_b32", 4: "layer_b128"}
+SDPA_KERNELS = {"offsets": ["k_plan_small", "k_plan_fill"], "qkt": ["k_qkt_bf16"], "softmax": ["k_softmax<true>"],
+                "attn_v": ["k_attn_v_bf16"]}
 
 
 def stage_work(T, d, H, dff, s2):
@@ -99,7 +109,8 @@ def source_hash(path):
 
 def load_traffic(kernel):
     """HBM bytes per launch measured with rocprofv3 counters (profiles/traffic.json),
-    only while the kernel's source is unchanged since the measurement."""
+    only while the kernel's source is unchanged since the measurement.  `kernel` may
+    carry a workload tag ("k_softmax<true>@layer_b128")."""
     path = os.path.join(ROOT, "profiles", "traffic.json")
     if not os.path.exists(path):
         return None
@@ -109,7 +120,7 @@ def load_traffic(kernel):
         return None
     if not rec:
         return None
-    src = KERNEL_SOURCES.get(kernel.split("<")[0])
+    src = KERNEL_SOURCES.get(kernel.split("@")[0].split("<")[0])
     if src is None or rec.get("source_sha") != source_hash(src):
         return None
     return rec.get("bytes_per_launch")
@@ -189,12 +200,13 @@ def _short(name):
     return base.split("(")[0].strip()
 
 
-def derive_traffic(fetch_csv, write_csv, cal_fetch_csv, cal_write_csv, copy_mib, kernels=None):
+def derive_traffic(fetch_csv, write_csv, cal_fetch_csv, cal_write_csv, copy_mib, kernels=None, tag=None):
     """HBM bytes per launch of every library kernel: FETCH_SIZE + WRITE_SIZE (KiB per
     dispatch), each scaled by copy_bytes / counter for a plain copy of known size.
     With `kernels` (base names, no template arguments), only those entries are replaced in the existing
     file, so each kernel's figure can come from a run in which all its dispatches
-    have the shape the bench line reports."""
+    have the shape the bench line reports.  With `tag`, entries are stored as
+    "name@tag" (one workload's dispatches of a symbol that runs at several shapes)."""
     fetch, write = _counter_per_dispatch(fetch_csv, "FETCH_SIZE"), _counter_per_dispatch(write_csv, "WRITE_SIZE")
     cf, cw = _counter_per_dispatch(cal_fetch_csv, "FETCH_SIZE"), _counter_per_dispatch(cal_write_csv, "WRITE_SIZE")
     big = lambda d: max(d.values())  # the copy kernel is the dispatch with the largest counts
@@ -203,14 +215,14 @@ def derive_traffic(fetch_csv, write_csv, cal_fetch_csv, cal_write_csv, copy_mib,
     out = {"_calibration": {"copy_mib": copy_mib, "fetch_scale": sf, "write_scale": sw,
                             "copy_fetch_kib": big(cf), "copy_write_kib": big(cw)}}
     path = os.path.join(ROOT, "profiles", "traffic.json")
-    if kernels is not None and os.path.exists(path):
+    if (kernels is not None or tag) and os.path.exists(path):
         out = {**json.load(open(path)), **out}
     for k in fetch:
         short = _short(k)
         src = KERNEL_SOURCES.get(short.split("<")[0])
         if src is None or (kernels is not None and short.split("<")[0] not in kernels):
             continue
-        out[short] = {"bytes_per_launch": round((fetch[k] * sf + write.get(k, 0.0) * sw) * 1024.0),
+        out[short + (f"@{tag}" if tag else "")] = {"bytes_per_launch": round((fetch[k] * sf + write.get(k, 0.0) * sw) * 1024.0),
                       "fetch_kib_raw": fetch[k], "write_kib_raw": write.get(k), "source_sha": source_hash(src)}
     with open(path, "w") as f:
         json.dump(out, f, indent=1, sort_keys=True)
@@ -318,6 +330,11 @@ def sdpa_measurement(rag, cid, seed=0, iters=30):
         if n in fl:
             o["useful_tflops"] = round(fl[n] / (t * 1e-3) / 1e12, 1)
             o["frac_of_bf16_peak"] = round(fl[n] / (t * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4)
+        hbm = [load_traffic(f"{k}@{SDPA_TAGS[cid]}") for k in SDPA_KERNELS[n]] if cid in SDPA_TAGS else [None]
+        if None not in hbm:  # counter-measured HBM bytes of the operator's kernels (one call)
+            o["hbm_bytes_per_call"] = sum(hbm)
+            o["hbm_GB_per_s"] = round(sum(hbm) / (t * 1e-3) / 1e9, 1)
+            o["hbm_frac_of_peak"] = round(sum(hbm) / (t * 1e-3) / 1e9 / PEAK_HBM_GBS, 4)
         ops[n] = o
     return {"workload": f"config {cid}: batch {cfg.batch}, lengths {cfg.lengths.replace(':', ' ')}, {H} heads x 64, bf16, "
                         f"T = {T}, {n_s} scores", "ops": ops,
@@ -527,6 +544,9 @@ def main():
     ap.add_argument("--layer-only", action="store_true",
                     help="time the layer steps only (no auxiliary measurements, no CPU baseline), so that a "
                          "profile of the run sees every dispatch of the layer's kernels at the layer's shape")
+    ap.add_argument("--ops-only", type=int, default=0, choices=(0, 2, 4), metavar="CONFIG",
+                    help="only time the unfused attention operators on configuration 2 or 4 and print their entry "
+                         "(the run a profile of those kernels uses)")
     ap.add_argument("--cpu-target-flops", type=float, default=2.0e10)
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of MIB MiB five times (counter calibration) and exit")
@@ -534,6 +554,7 @@ def main():
                     help="turn rocprofv3 --pmc FETCH_SIZE / WRITE_SIZE counter files of a bench run and of a "
                          "copy-calibration run into profiles/traffic.json, then exit")
     ap.add_argument("--copy-mib", type=int, default=512, help="size of the calibration copy (for --derive-traffic)")
+    ap.add_argument("--traffic-tag", default=None, help="store --derive-traffic entries as name@TAG")
     ap.add_argument("--traffic-kernels", default=None,
                     help="comma-separated kernel base names (e.g. k_vgemm_bf16): --derive-traffic replaces only their entries")
     args = ap.parse_args()
@@ -542,7 +563,7 @@ def main():
         args.no_configs = args.no_peaks = args.no_cpu_baseline = True
     if args.derive_traffic:
         kernels = set(args.traffic_kernels.split(",")) if args.traffic_kernels else None
-        derive_traffic(*args.derive_traffic, copy_mib=args.copy_mib, kernels=kernels)
+        derive_traffic(*args.derive_traffic, copy_mib=args.copy_mib, kernels=kernels, tag=args.traffic_tag)
         return
     if args.copy_calibration:
         import torch
@@ -567,6 +588,9 @@ def main():
     from workloads import BIAS_NAMES, LN_NAMES, WEIGHT_NAMES, make_workload
 
     torch.cuda.set_device(0)
+    if args.ops_only:
+        print(json.dumps({SDPA_TAGS[args.ops_only]: sdpa_measurement(rag, args.ops_only)}))
+        return
     wl = make_workload(args.config, seed=args.seed)
     cfg = wl.cfg
     L = wl.lengths
