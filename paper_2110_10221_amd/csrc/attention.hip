@@ -408,6 +408,9 @@ typedef __attribute__((address_space(3))) void lds_void_t;
 typedef __attribute__((ext_vector_type(4))) short short4_t;
 typedef __attribute__((address_space(3))) short4_t lds_short4_t;
 
+#ifndef RAG_ATTN_SNAKE
+#define RAG_ATTN_SNAKE 1
+#endif
 #ifndef RAG_ATTN_WAVES
 #define RAG_ATTN_WAVES 16
 #endif
@@ -465,7 +468,15 @@ void k_attention_bf16(PlanArgs pa, const int32_t* __restrict__ order, const uint
     const float zs = fabsf(scale) * 1.4426950408889634f;
     const uint32_t qsign = scale < 0.f ? 0x80008000u : 0u;
 
-    for (int pair = blockIdx.x; pair < n_pairs; pair += gridDim.x) {
+    for (int round = 0; round * (int)gridDim.x < n_pairs; ++round) {
+#if RAG_ATTN_SNAKE
+        // pairs are dealt in a snake (workgroups 0..G-1, then G-1..0, ...): with the
+        // list longest first, every workgroup's sum of pair costs is then about equal
+        const int pair = round * gridDim.x + ((round & 1) ? gridDim.x - 1 - blockIdx.x : blockIdx.x);
+#else
+        const int pair = round * gridDim.x + blockIdx.x;
+#endif
+        if (pair >= n_pairs) continue;
         const int b = order[pair / H], h = pair % H;
         const int L = pa.lengths[b];
         if (L == 0) continue;
