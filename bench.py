@@ -60,13 +60,14 @@ KERNEL_SOURCES = {
     "k_qkt_bf16": "paper_2110_10221_amd/csrc/attention.hip",
     "k_softmax": "paper_2110_10221_amd/csrc/attention.hip",
     "k_attn_v_bf16": "paper_2110_10221_amd/csrc/attention.hip",
+    "k_plan_fused": "paper_2110_10221_amd/csrc/offsets.hip",
     "k_plan_small": "paper_2110_10221_amd/csrc/offsets.hip",
     "k_plan_fill": "paper_2110_10221_amd/csrc/offsets.hip",
 }
 # unfused operator measurements: kernels of each operator, and the tag under which
 # their counters are stored per workload (the same symbols run at both shapes)
 SDPA_TAGS = {2: "sdpa_b32", 4: "layer_b128"}
-SDPA_KERNELS = {"offsets": ["k_plan_small", "k_plan_fill"], "qkt": ["k_qkt_bf16"], "softmax": ["k_softmax<true>"],
+SDPA_KERNELS = {"offsets": ["k_plan_fused"], "qkt": ["k_qkt_bf16"], "softmax": ["k_softmax<true>"],
                 "attn_v": ["k_attn_v_bf16"]}
 
 
@@ -338,7 +339,8 @@ def sdpa_measurement(rag, cid, seed=0, iters=30):
         ops[n] = o
     return {"workload": f"config {cid}: batch {cfg.batch}, lengths {cfg.lengths.replace(':', ' ')}, {H} heads x 64, bf16, "
                         f"T = {T}, {n_s} scores", "ops": ops,
-            "kernels": {"offsets": "k_plan_small + k_plan_fill" if len(L) <= 1024 else "k_plan_scan/rank/items/fill",
+            "kernels": {"offsets": "k_plan_fused" if len(L) <= 256 else
+                        "k_plan_small + k_plan_fill" if len(L) <= 1024 else "k_plan_scan/rank/items/fill",
                         "qkt": "k_qkt_bf16", "softmax": "k_softmax<true>", "attn_v": "k_attn_v_bf16"}}
 
 
