@@ -408,6 +408,15 @@ typedef __attribute__((address_space(3))) void lds_void_t;
 typedef __attribute__((ext_vector_type(4))) short short4_t;
 typedef __attribute__((address_space(3))) short4_t lds_short4_t;
 
+#ifndef RAG_STREAM_PER_CU
+#define RAG_STREAM_PER_CU 64
+#endif
+#ifndef RAG_ATTN_TR_ASM
+#define RAG_ATTN_TR_ASM 1
+#endif
+#ifndef RAG_ATTN_STREAM
+#define RAG_ATTN_STREAM 1
+#endif
 #ifndef RAG_ATTN_SNAKE
 #define RAG_ATTN_SNAKE 1
 #endif
@@ -606,6 +615,199 @@ void k_attention_bf16(PlanArgs pa, const int32_t* __restrict__ order, const uint
     }
 }
 
+// Streaming variant: one (sequence b, head h, 64-query tile) item of the plan's
+// Attn.V list per workgroup of two waves (32 queries each).  The keys stream
+// through two LDS stages of 32 K rows and 32 V rows (16 KB per workgroup), so
+// eight workgroups share a CU: while one waits for its next chunk, the others
+// compute, and every SIMD keeps four busy waves whatever the sequence lengths.
+// The per-chunk arithmetic is the pair kernel's above.  Items are dealt to the
+// XCDs in runs of kStreamRun consecutive list entries (a sequence's tiles of one
+// head share its K / V rows in that XCD's L2), the runs round-robin.
+constexpr int kStreamWaves = 2, kStreamThreads = kStreamWaves * kWave;
+constexpr int kStreamChunk = 32;                                // keys per LDS stage
+constexpr int kStreamStageElems = 2 * kStreamChunk * kHeadDim;  // K rows, then V rows
+constexpr int kStreamRun = 8;
+
+__device__ __forceinline__ int stream_item(int bid, int nb) {  // nb: a multiple of 8 * kStreamRun
+    const int xcd = bid % 8, j = bid / 8;
+    return ((j / kStreamRun) * 8 + xcd) * kStreamRun + j % kStreamRun;
+}
+
+template <bool CAUSAL>
+__global__ __launch_bounds__(kStreamThreads) __attribute__((amdgpu_waves_per_eu(4)))
+void k_attention_stream_bf16(PlanArgs pa, const uint16_t* __restrict__ q, int ldq, const uint16_t* __restrict__ k,
+                             int ldk, const uint16_t* __restrict__ v, int ldv, float scale,
+                             uint16_t* __restrict__ O, int ldo) {
+    if (pa.status[0] != 0) return;
+    __shared__ __attribute__((aligned(16))) uint16_t kvs[2 * kStreamStageElems];
+    const int n_items = pa.status[2];
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave), lane = threadIdx.x % kWave;
+    const int l32 = lane % 32, h2 = lane / 32;
+    const int tr_e = (lane % 16) / 4, tr_q = lane % 4, tr_g = lane / 16;
+    const float zs = fabsf(scale) * 1.4426950408889634f;
+    const uint32_t qsign = scale < 0.f ? 0x80008000u : 0u;
+    // a stage holds keys 32c .. 32c + 31 at rows 0..31; 32c leaves the swizzle's
+    // row bits 1-3 unchanged, so the offsets are those of chunk 0
+    int koff[4], voff[2][2];
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) koff[ks] = kv_off(l32, 16 * ks + 8 * h2);
+#pragma unroll
+    for (int cb = 0; cb < 2; ++cb)
+#pragma unroll
+        for (int hi = 0; hi < 2; ++hi)
+            voff[cb][hi] = kv_off(4 * (tr_g >> 1) + tr_e + 8 * hi, 32 * cb + 16 * (tr_g & 1) + 4 * tr_q);
+
+    for (int base = 0; base < n_items; base += gridDim.x) {
+        const int it = base + stream_item(blockIdx.x, gridDim.x);
+        if (it >= n_items) break;
+        const int b = pa.av_items[3 * it], h = pa.av_items[3 * it + 1], ti = pa.av_items[3 * it + 2];
+        const int L = pa.lengths[b];
+        const int t0 = pa.tok_off[b];
+        const int qb = 2 * ti + wave;  // this wave's 32-query block
+        const bool active = qb * 32 < L;
+        const int nc_all = (L + 31) / 32;
+        const int nc_wg = CAUSAL ? min(nc_all, 2 * ti + 2) : nc_all;  // chunks the workgroup loads
+        const int nc_me = CAUSAL ? qb + 1 : nc_all;                    // chunks this wave uses
+        const __amdgpu_buffer_rsrc_t rk = __builtin_amdgcn_make_buffer_rsrc(
+            const_cast<uint16_t*>(k + (int64_t)t0 * ldk + h * kHeadDim), 0, (uint32_t)L * ldk * 2u, 0x00020000);
+        const __amdgpu_buffer_rsrc_t rv = __builtin_amdgcn_make_buffer_rsrc(
+            const_cast<uint16_t*>(v + (int64_t)t0 * ldv + h * kHeadDim), 0, (uint32_t)L * ldv * 2u, 0x00020000);
+        // wave w copies rows 16w .. 16w + 15 of the chunk's K and V (two 1 KB blocks
+        // of 8 rows each); rows past L arrive as zeros
+        auto issue = [&](int c) {
+            uint16_t* st = kvs + (c & 1) * kStreamStageElems;
+#pragma unroll
+            for (int i = 0; i < 2; ++i) {
+                const int blk = wave * 2 + i;
+                const int row = c * kStreamChunk + blk * 8 + lane / 8;
+                const int logical = (lane % 8) ^ kv_swz(row);
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(rk, (lds_void_t*)(st + blk * 512), 16,
+                                                         row * ldk * 2 + logical * 16, 0, 0, 0);
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(rv, (lds_void_t*)(st + kStreamChunk * kHeadDim + blk * 512),
+                                                         16, row * ldv * 2 + logical * 16, 0, 0, 0);
+            }
+        };
+        bf16x8 qf[4];
+        {
+            const int qi = min(qb * 32 + l32, L - 1);
+            const uint16_t* qrow = q + (int64_t)(t0 + qi) * ldq + h * kHeadDim + 8 * h2;
+#pragma unroll
+            for (int ks = 0; ks < 4; ++ks) {
+                u32x4 raw = active ? ld16(qrow + 16 * ks) : u32x4{0u, 0u, 0u, 0u};
+                raw ^= qsign;
+                qf[ks] = as_bf16x8(raw);
+            }
+        }
+        float m = -INFINITY, lsum = 0.f;
+        floatx16 oacc[2];
+#pragma unroll
+        for (int cb = 0; cb < 2; ++cb)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) oacc[cb][r] = 0.f;
+        attn_barrier();  // both stages are free: the previous item's reads are done
+        issue(0);
+        for (int c = 0; c < nc_wg; ++c) {
+            asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // this wave's copies of chunk c
+            attn_barrier();  // ... and the other wave's; chunk c + 1's stage was last read in step c - 1
+            if (c + 1 < nc_wg) issue(c + 1);
+            if (!active || c >= nc_me) continue;
+            const uint16_t* kp = kvs + (c & 1) * kStreamStageElems + koff[0];
+            const uint16_t* vp = kvs + (c & 1) * kStreamStageElems + kStreamChunk * kHeadDim;
+            floatx16 acc;
+#pragma unroll
+            for (int r = 0; r < 16; ++r) acc[r] = 0.f;
+            bf16x8 kf[4];
+#pragma unroll
+            for (int ks = 0; ks < 4; ++ks)
+                kf[ks] = as_bf16x8(*reinterpret_cast<const u32x4*>(kp + (koff[ks] - koff[0])));
+            __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+            for (int ks = 0; ks < 4; ++ks) acc = mfma32x32x16(kf[ks], qf[ks], acc);
+            if (32 * (c + 1) > L || (CAUSAL && c == qb)) {
+                const int kmax = CAUSAL && c == qb ? min(L - 1, qb * 32 + l32) : L - 1;
+#pragma unroll
+                for (int r = 0; r < 16; ++r)
+                    if (32 * c + 8 * (r / 4) + 4 * h2 + (r % 4) > kmax) acc[r] = -INFINITY;
+            }
+            float cmax = acc[0];
+#pragma unroll
+            for (int r = 1; r < 16; ++r) cmax = fmaxf(cmax, acc[r]);
+            const float cz = max_xor32(cmax) * zs;
+            const bool raise = cz > m + kRescaleSlack;
+            if (__ballot(raise) != 0) {
+                const float mn = raise ? cz : m;
+                const float alpha = raise ? __builtin_amdgcn_exp2f(m - mn) : 1.f;
+                lsum *= alpha;
+#pragma unroll
+                for (int cb = 0; cb < 2; ++cb)
+#pragma unroll
+                    for (int r = 0; r < 16; ++r) oacc[cb][r] *= alpha;
+                m = mn;
+            }
+#pragma unroll
+            for (int t = 0; t < 2; ++t) {
+                u32x4 pw;
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const float e0 = __builtin_amdgcn_exp2f(fmaf(acc[8 * t + 2 * e], zs, -m));
+                    const float e1 = __builtin_amdgcn_exp2f(fmaf(acc[8 * t + 2 * e + 1], zs, -m));
+                    lsum += e0 + e1;
+                    pw[e] = pack_bf16x2(e0, e1);
+                }
+                const bf16x8 pb = as_bf16x8(pw);
+#if RAG_ATTN_TR_ASM
+                // the transposed reads as inline assembly: the builtin makes the compiler
+                // wait for every LDS copy in flight first, chunk c + 1's included
+                // (one statement with its wait, so no result is used before it lands)
+                const uint16_t* vt = vp + 16 * t * kHeadDim;
+                u32x2 tr[2][2];
+                asm volatile(
+                    "ds_read_b64_tr_b16 %0, %4\n\t"
+                    "ds_read_b64_tr_b16 %1, %5\n\t"
+                    "ds_read_b64_tr_b16 %2, %6\n\t"
+                    "ds_read_b64_tr_b16 %3, %7\n\t"
+                    "s_waitcnt lgkmcnt(0)"
+                    : "=&v"(tr[0][0]), "=&v"(tr[0][1]), "=&v"(tr[1][0]), "=&v"(tr[1][1])
+                    : "v"((uint32_t)(uintptr_t)(vt + voff[0][0])), "v"((uint32_t)(uintptr_t)(vt + voff[0][1])),
+                      "v"((uint32_t)(uintptr_t)(vt + voff[1][0])), "v"((uint32_t)(uintptr_t)(vt + voff[1][1]))
+                    : "memory");
+#pragma unroll
+                for (int cb = 0; cb < 2; ++cb)
+                    oacc[cb] = mfma32x32x16(as_bf16x8(u32x4{tr[cb][0][0], tr[cb][0][1], tr[cb][1][0], tr[cb][1][1]}), pb,
+                                            oacc[cb]);
+#else
+#pragma unroll
+                for (int cb = 0; cb < 2; ++cb) {
+                    const uint16_t* vt = vp + 16 * t * kHeadDim;
+                    const short4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_short4_t*)(vt + voff[cb][0]));
+                    const short4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_short4_t*)(vt + voff[cb][1]));
+                    const u32x4 va = {(uint32_t)(uint16_t)lo[0] | ((uint32_t)(uint16_t)lo[1] << 16),
+                                      (uint32_t)(uint16_t)lo[2] | ((uint32_t)(uint16_t)lo[3] << 16),
+                                      (uint32_t)(uint16_t)hi[0] | ((uint32_t)(uint16_t)hi[1] << 16),
+                                      (uint32_t)(uint16_t)hi[2] | ((uint32_t)(uint16_t)hi[3] << 16)};
+                    oacc[cb] = mfma32x32x16(as_bf16x8(va), pb, oacc[cb]);
+                }
+#endif
+            }
+        }
+        if (active) {
+            const float inv = 1.0f / sum_xor32(lsum);
+            const int i = qb * 32 + l32;
+            if (i < L) {
+                uint16_t* orow = O + (int64_t)(t0 + i) * ldo + h * kHeadDim;
+#pragma unroll
+                for (int cb = 0; cb < 2; ++cb)
+#pragma unroll
+                    for (int g = 0; g < 4; ++g) {
+                        const u32x2 w2 = {pack_bf16x2(oacc[cb][4 * g] * inv, oacc[cb][4 * g + 1] * inv),
+                                          pack_bf16x2(oacc[cb][4 * g + 2] * inv, oacc[cb][4 * g + 3] * inv)};
+                        *reinterpret_cast<u32x2*>(orow + 32 * cb + 8 * g + 4 * h2) = w2;
+                    }
+            }
+        }
+    }
+}
+
 int persistent_grid(int64_t cap, int per_cu) {
     const int64_t g = (int64_t)device_cu_count() * per_cu;
     return static_cast<int>(cap < g ? (cap > 0 ? cap : 1) : g);
@@ -667,6 +869,20 @@ hipError_t launch_fused_variant(const PlanView& p, const void* q, int ldq, const
         attr_set = true;
     }
     const PlanArgs pa = plan_args(p);
+#if RAG_ATTN_STREAM
+    {
+        // one workgroup per item, at most 64 per CU (the workgroups then loop over
+        // the list); a multiple of 8 * kStreamRun so the XCD dealing is a permutation
+        constexpr int64_t kUnit = 8 * kStreamRun;
+        const int64_t cap = std::max<int64_t>(p.av_cap, 1);
+        const int64_t limit = (int64_t)device_cu_count() * RAG_STREAM_PER_CU;
+        const int64_t g = (std::min(cap, limit) + kUnit - 1) / kUnit * kUnit;
+        hipLaunchKernelGGL(k_attention_stream_bf16<CAUSAL>, dim3((unsigned)g), dim3(kStreamThreads), 0, s, pa,
+                           static_cast<const uint16_t*>(q), ldq, static_cast<const uint16_t*>(k), ldk,
+                           static_cast<const uint16_t*>(v), ldv, scale, static_cast<uint16_t*>(out), ldo);
+        return hipGetLastError();
+    }
+#endif
     const int64_t pairs = (int64_t)p.batch * p.heads;
     const int grid = static_cast<int>(std::min<int64_t>(pairs, device_cu_count()));
     hipLaunchKernelGGL(k_attention_bf16<CAUSAL>, dim3(grid), dim3(kAttnThreads), kAttnLds, s, pa, p.order,
