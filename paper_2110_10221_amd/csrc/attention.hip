@@ -656,6 +656,13 @@ void k_attention_stream_bf16(PlanArgs pa, const uint16_t* __restrict__ q, int ld
 #pragma unroll
         for (int hi = 0; hi < 2; ++hi)
             voff[cb][hi] = kv_off(4 * (tr_g >> 1) + tr_e + 8 * hi, 32 * cb + 16 * (tr_g & 1) + 4 * tr_q);
+    // LDS byte addresses of the transposed V reads in stage 0, key step 0
+    uint32_t vaddr[2][2];
+#pragma unroll
+    for (int cb = 0; cb < 2; ++cb)
+#pragma unroll
+        for (int hi = 0; hi < 2; ++hi)
+            vaddr[cb][hi] = (uint32_t)(uintptr_t)(kvs + kStreamChunk * kHeadDim + voff[cb][hi]);
 
     for (int base = 0; base < n_items; base += gridDim.x) {
         const int it = base + stream_item(blockIdx.x, gridDim.x);
@@ -673,18 +680,25 @@ void k_attention_stream_bf16(PlanArgs pa, const uint16_t* __restrict__ q, int ld
         const __amdgpu_buffer_rsrc_t rv = __builtin_amdgcn_make_buffer_rsrc(
             const_cast<uint16_t*>(v + (int64_t)t0 * ldv + h * kHeadDim), 0, (uint32_t)L * ldv * 2u, 0x00020000);
         // wave w copies rows 16w .. 16w + 15 of the chunk's K and V (two 1 KB blocks
-        // of 8 rows each); rows past L arrive as zeros
-        auto issue = [&](int c) {
-            uint16_t* st = kvs + (c & 1) * kStreamStageElems;
+        // of 8 rows each); rows past L arrive as zeros.  Chunk c adds 32c rows to
+        // the lane offsets of chunk 0 (32c leaves the swizzle's row bits alone).
+        int vko[2], vvo[2];
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {
+            const int row = (wave * 2 + i) * 8 + lane / 8;
+            const int logical = (lane % 8) ^ kv_swz(row);
+            vko[i] = row * ldk * 2 + logical * 16;
+            vvo[i] = row * ldv * 2 + logical * 16;
+        }
+        auto issue = [&](int c, auto stg) {
+            uint16_t* st = kvs + decltype(stg)::value * kStreamStageElems;
+            const int dk = c * kStreamChunk * ldk * 2, dv = c * kStreamChunk * ldv * 2;
 #pragma unroll
             for (int i = 0; i < 2; ++i) {
                 const int blk = wave * 2 + i;
-                const int row = c * kStreamChunk + blk * 8 + lane / 8;
-                const int logical = (lane % 8) ^ kv_swz(row);
-                __builtin_amdgcn_raw_ptr_buffer_load_lds(rk, (lds_void_t*)(st + blk * 512), 16,
-                                                         row * ldk * 2 + logical * 16, 0, 0, 0);
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(rk, (lds_void_t*)(st + blk * 512), 16, vko[i] + dk, 0, 0, 0);
                 __builtin_amdgcn_raw_ptr_buffer_load_lds(rv, (lds_void_t*)(st + kStreamChunk * kHeadDim + blk * 512),
-                                                         16, row * ldv * 2 + logical * 16, 0, 0, 0);
+                                                         16, vvo[i] + dv, 0, 0, 0);
             }
         };
         bf16x8 qf[4];
@@ -704,22 +718,21 @@ void k_attention_stream_bf16(PlanArgs pa, const uint16_t* __restrict__ q, int ld
         for (int cb = 0; cb < 2; ++cb)
 #pragma unroll
             for (int r = 0; r < 16; ++r) oacc[cb][r] = 0.f;
-        attn_barrier();  // both stages are free: the previous item's reads are done
-        issue(0);
-        for (int c = 0; c < nc_wg; ++c) {
+        // chunk c in stage STG (c's parity, a compile-time constant, so every LDS
+        // address is a fixed per-lane register plus an immediate offset)
+        auto step = [&](int c, auto stg) {
+            constexpr int STG = decltype(stg)::value;
             asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // this wave's copies of chunk c
             attn_barrier();  // ... and the other wave's; chunk c + 1's stage was last read in step c - 1
-            if (c + 1 < nc_wg) issue(c + 1);
-            if (!active || c >= nc_me) continue;
-            const uint16_t* kp = kvs + (c & 1) * kStreamStageElems + koff[0];
-            const uint16_t* vp = kvs + (c & 1) * kStreamStageElems + kStreamChunk * kHeadDim;
+            if (c + 1 < nc_wg) issue(c + 1, std::integral_constant<int, 1 - STG>{});
+            if (!active || c >= nc_me) return;
+            const uint16_t* kst = kvs + STG * kStreamStageElems;
             floatx16 acc;
 #pragma unroll
             for (int r = 0; r < 16; ++r) acc[r] = 0.f;
             bf16x8 kf[4];
 #pragma unroll
-            for (int ks = 0; ks < 4; ++ks)
-                kf[ks] = as_bf16x8(*reinterpret_cast<const u32x4*>(kp + (koff[ks] - koff[0])));
+            for (int ks = 0; ks < 4; ++ks) kf[ks] = as_bf16x8(*reinterpret_cast<const u32x4*>(kst + koff[ks]));
             __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
             for (int ks = 0; ks < 4; ++ks) acc = mfma32x32x16(kf[ks], qf[ks], acc);
@@ -755,40 +768,31 @@ void k_attention_stream_bf16(PlanArgs pa, const uint16_t* __restrict__ q, int ld
                     pw[e] = pack_bf16x2(e0, e1);
                 }
                 const bf16x8 pb = as_bf16x8(pw);
-#if RAG_ATTN_TR_ASM
-                // the transposed reads as inline assembly: the builtin makes the compiler
-                // wait for every LDS copy in flight first, chunk c + 1's included
-                // (one statement with its wait, so no result is used before it lands)
-                const uint16_t* vt = vp + 16 * t * kHeadDim;
+                // V^T operand by transposed reads, as inline assembly with its wait in
+                // the same statement: the builtin makes the compiler first wait for
+                // every LDS copy in flight, chunk c + 1's included
                 u32x2 tr[2][2];
                 asm volatile(
-                    "ds_read_b64_tr_b16 %0, %4\n\t"
-                    "ds_read_b64_tr_b16 %1, %5\n\t"
-                    "ds_read_b64_tr_b16 %2, %6\n\t"
-                    "ds_read_b64_tr_b16 %3, %7\n\t"
+                    "ds_read_b64_tr_b16 %0, %4 offset:%8\n\t"
+                    "ds_read_b64_tr_b16 %1, %5 offset:%8\n\t"
+                    "ds_read_b64_tr_b16 %2, %6 offset:%8\n\t"
+                    "ds_read_b64_tr_b16 %3, %7 offset:%8\n\t"
                     "s_waitcnt lgkmcnt(0)"
                     : "=&v"(tr[0][0]), "=&v"(tr[0][1]), "=&v"(tr[1][0]), "=&v"(tr[1][1])
-                    : "v"((uint32_t)(uintptr_t)(vt + voff[0][0])), "v"((uint32_t)(uintptr_t)(vt + voff[0][1])),
-                      "v"((uint32_t)(uintptr_t)(vt + voff[1][0])), "v"((uint32_t)(uintptr_t)(vt + voff[1][1]))
+                    : "v"(vaddr[0][0]), "v"(vaddr[0][1]), "v"(vaddr[1][0]), "v"(vaddr[1][1]),
+                      "i"((STG * kStreamStageElems + 16 * t * kHeadDim) * 2)
                     : "memory");
 #pragma unroll
                 for (int cb = 0; cb < 2; ++cb)
                     oacc[cb] = mfma32x32x16(as_bf16x8(u32x4{tr[cb][0][0], tr[cb][0][1], tr[cb][1][0], tr[cb][1][1]}), pb,
                                             oacc[cb]);
-#else
-#pragma unroll
-                for (int cb = 0; cb < 2; ++cb) {
-                    const uint16_t* vt = vp + 16 * t * kHeadDim;
-                    const short4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_short4_t*)(vt + voff[cb][0]));
-                    const short4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_short4_t*)(vt + voff[cb][1]));
-                    const u32x4 va = {(uint32_t)(uint16_t)lo[0] | ((uint32_t)(uint16_t)lo[1] << 16),
-                                      (uint32_t)(uint16_t)lo[2] | ((uint32_t)(uint16_t)lo[3] << 16),
-                                      (uint32_t)(uint16_t)hi[0] | ((uint32_t)(uint16_t)hi[1] << 16),
-                                      (uint32_t)(uint16_t)hi[2] | ((uint32_t)(uint16_t)hi[3] << 16)};
-                    oacc[cb] = mfma32x32x16(as_bf16x8(va), pb, oacc[cb]);
-                }
-#endif
             }
+        };
+        attn_barrier();  // both stages are free: the previous item's reads are done
+        issue(0, std::integral_constant<int, 0>{});
+        for (int c = 0; c < nc_wg; c += 2) {
+            step(c, std::integral_constant<int, 0>{});
+            if (c + 1 < nc_wg) step(c + 1, std::integral_constant<int, 1>{});
         }
         if (active) {
             const float inv = 1.0f / sum_xor32(lsum);
