@@ -67,8 +67,6 @@ enum { RAG_ACT_NONE = 0, RAG_ACT_GELU_ERF = 1, RAG_ACT_GELU_TANH = 2 };
 #define RAG_MAX_BATCH 65536
 /* The only head dimension the kernels are built for. */
 #define RAG_HEAD_DIM 64
-/* Longest sequence (plan max_len) the fused attention kernel accepts. */
-#define RAG_FUSED_MAX_LEN 512
 
 /* Bits of status[0]. */
 enum {
@@ -194,15 +192,17 @@ rag_status ragged_attn_v(const rag_plan* plan, const void* probs, int64_t score_
                          void* stream);
 
 /*
- * Fused ragged attention (bf16, plan max_len <= RAG_FUSED_MAX_LEN): the
- * composition of ragged_qkt, ragged_softmax and ragged_attn_v,
+ * Fused ragged attention (bf16, any sequence length): the composition of
+ * ragged_qkt, ragged_softmax and ragged_attn_v,
  *   out[t_i][h*hd + c] = sum_j softmax_j(scale * q_i . k_j) v[t_j][h*hd + c],
  * computed per (sequence, head) in one pass over the keys without storing
  * scores or probabilities: fp32 scores, an online softmax, bf16 unnormalised
  * exponentials as the operand of the P.V product and one division by the row
- * sum (so it differs from the three operators by rounding only).  Same operand
- * rules as the three operators; RAG_ERR_DTYPE unless bf16, RAG_ERR_SHAPE if
- * max_len is too long.
+ * sum (so it differs from the three operators by rounding only).  The keys
+ * stream through LDS in chunks, so no length limit applies beyond 32-bit byte
+ * offsets within a sequence.  Same operand rules as the three operators;
+ * RAG_ERR_DTYPE unless bf16, RAG_ERR_SHAPE if max_len * max(ldk, ldv) * 2
+ * exceeds 2^31 - 1.
  */
 rag_status ragged_attention(const rag_plan* plan, const void* q, int32_t ldq, const void* k, int32_t ldk,
                             const void* v, int32_t ldv, int32_t head_dim, float scale, void* out,
@@ -381,9 +381,9 @@ enum {
 
 /*
  * (host only)  Workspace bytes encoder_layer needs for these sizes.  With
- * RAG_LAYER_UNFUSED_ATTENTION, and always for RAG_F32 or max_len >
- * RAG_FUSED_MAX_LEN (where the fused attention kernel does not apply), the
- * score buffer is sized for the worst case H * T * max_len.
+ * RAG_LAYER_UNFUSED_ATTENTION, and always for RAG_F32 or max_len * 3 * d_model
+ * * 2 > 2^31 - 1 (where the fused attention kernel does not apply), the score
+ * buffer is sized for the worst case H * T * max_len.
  */
 rag_status encoder_layer_workspace(int32_t total_tokens, int32_t max_len, int32_t d_model,
                                    int32_t heads, int32_t d_ff, int32_t dtype, int32_t flags,

@@ -57,6 +57,10 @@ rag_status finish(hipError_t launch_err, hipStream_t s, const int32_t* status, c
     return RAG_OK;
 }
 
+// The fused attention kernel addresses a sequence's K and V rows with 32-bit
+// byte offsets from the sequence's first row.
+bool fused_fits(int64_t max_len, int64_t ld) { return max_len * ld * 2 <= INT32_MAX; }
+
 rag_status view_plan(const rag_plan* p, rag::PlanView& v, const char* fn) {
     if (!p) return fail(RAG_ERR_ARG, "%s: plan is NULL", fn);
     if (p->batch < 1 || p->batch > RAG_MAX_BATCH)
@@ -223,13 +227,14 @@ rag_status attention_impl(const rag_plan* plan, const void* q, int32_t ldq, cons
     rag_status st;
     if ((st = view_plan(plan, v, fn)) || (st = check_dtype(dtype, fn))) return st;
     if (dtype != RAG_BF16) return fail(RAG_ERR_DTYPE, "%s: the fused kernel is bf16 only", fn);
-    if (plan->max_len > RAG_FUSED_MAX_LEN)
-        return fail(RAG_ERR_SHAPE, "%s: max_len %d exceeds %d", fn, plan->max_len, RAG_FUSED_MAX_LEN);
     if (head_dim != RAG_HEAD_DIM) return fail(RAG_ERR_SHAPE, "%s: head_dim %d unsupported (only %d)", fn, head_dim, RAG_HEAD_DIM);
     const int64_t width = (int64_t)plan->heads * head_dim;
     if ((st = check_operand(q, ldq, width, dtype, 16, "q", fn)) || (st = check_operand(k, ldk, width, dtype, 16, "k", fn)) ||
         (st = check_operand(vv, ldv, width, dtype, 16, "v", fn)) || (st = check_operand(out, ldo, width, dtype, 16, "out", fn)))
         return st;
+    if (!fused_fits(plan->max_len, ldk > ldv ? ldk : ldv))
+        return fail(RAG_ERR_SHAPE, "%s: max_len %d rows of leading dimension %d exceed the kernel's 32-bit offsets", fn,
+                    plan->max_len, ldk > ldv ? ldk : ldv);
     hipStream_t s = static_cast<hipStream_t>(stream);
     return finish(rag::launch_fused_attention(v, dtype, q, ldq, k, ldk, vv, ldv, scale, out, ldo, causal, s), s,
                   plan->status, fn);
@@ -358,11 +363,12 @@ namespace {
 constexpr size_t kAlign = 256;
 size_t round_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
 
-// The fused attention kernel exists for bf16 and sequences of up to
-// RAG_FUSED_MAX_LEN tokens; other layers run the three attention operators over
-// a materialised score buffer.
-bool unfused_attention(int32_t dtype, int32_t flags, int64_t max_len) {
-    return (flags & RAG_LAYER_UNFUSED_ATTENTION) || dtype == RAG_F32 || max_len > RAG_FUSED_MAX_LEN;
+// The fused attention kernel exists for bf16 (and sequences whose K / V rows its
+// 32-bit offsets reach); other layers run the three attention operators over a
+// materialised score buffer.  The layer's Q, K and V are column blocks of one
+// [T, 3d] buffer.
+bool unfused_attention(int32_t dtype, int32_t flags, int64_t max_len, int64_t d) {
+    return (flags & RAG_LAYER_UNFUSED_ATTENTION) || dtype == RAG_F32 || !fused_fits(max_len, 3 * d);
 }
 
 struct LayerBuffers {
@@ -376,7 +382,7 @@ LayerBuffers layer_buffers(int64_t T, int64_t max_len, int64_t d, int64_t H, int
     lb.qkvf = round_up((size_t)T * (size_t)(3 * d > d_ff ? 3 * d : d_ff) * es);  // QKV, later FF1 output
     lb.act_a = round_up((size_t)T * d * es);                                     // Y1, later Y2
     lb.h1o = round_up((size_t)T * d * es);                                       // attention output, later H1
-    lb.scores = unfused_attention(dtype, flags, max_len) ? round_up((size_t)H * T * max_len * es) : 0;
+    lb.scores = unfused_attention(dtype, flags, max_len, d) ? round_up((size_t)H * T * max_len * es) : 0;
     lb.total = lb.qkvf + lb.act_a + lb.h1o + lb.scores;
     return lb;
 }
@@ -447,7 +453,7 @@ rag_status encoder_layer(const rag_plan* plan, const void* x, void* y, int32_t d
     mark(0);
     run(rag::launch_linear(dtype, x, d, w->w_qkv, w->b_qkv, nullptr, 0, RAG_ACT_NONE, qkv, 3 * d, T, d, 3 * d, s));
     mark(1);
-    if (unfused_attention(dtype, flags, plan->max_len)) {
+    if (unfused_attention(dtype, flags, plan->max_len, d)) {
         const int64_t cap = (int64_t)(lb.scores / es);
         run(rag::launch_qkt(v, dtype, qkvc, 3 * d, qkvc + es * d, 3 * d, scale, scores, cap, causal, s));
         mark(2);

@@ -376,16 +376,16 @@ __global__ __launch_bounds__(256) void k_attn_v_f32(PlanArgs pa, const float* __
     }
 }
 
-
 // ---------------------------------------------------------------------------
-// Fused ragged attention: QK^T, softmax and Attn.V of one (sequence b, head h)
-// pair per workgroup of sixteen waves (four per SIMD) in a single pass over
-// the keys; no score reaches memory.
-//   load   the pair's K and V rows (at most RAG_FUSED_MAX_LEN of them) are
-//          copied once into LDS with bounds-checked buffer loads that write
-//          LDS directly (16-byte chunks XOR-swizzled by row)
-//   then each wave takes 32-query blocks of the sequence in turn and walks the
-//   keys 32 at a time:
+// Fused ragged attention: QK^T, softmax and Attn.V in one pass over the keys; no
+// score reaches memory.  One (sequence b, head h, 64-query tile) item of the
+// plan's Attn.V list per workgroup of two waves, 32 queries per wave, items
+// longest sequence first (the plan's order).
+//   keys   stream through two LDS stages of 32 K rows and 32 V rows (16 KB per
+//          workgroup, so eight workgroups share a CU: while one waits for its
+//          next chunk the others compute, and every SIMD keeps four busy waves
+//          whatever the lengths); bounds-checked buffer loads write LDS
+//          directly, 16-byte chunks XOR-swizzled by row, rows past L_b as zeros
 //   scores S^T = K Q^T with v_mfma_f32_32x32x16_bf16 (lane holds query
 //          i = lane % 32 and keys 8*(r/4) + 4*(lane/32) + r%4), kept in fp32
 //   softmax online: z = s * scale * log2(e); a per-row reference m, raised
@@ -400,34 +400,25 @@ __global__ __launch_bounds__(256) void k_attn_v_f32(PlanArgs pa, const float* __
 // Relative to the three separate operators, the fused path skips the bf16
 // rounding of the scores and rounds the unnormalised exponentials instead of
 // the probabilities (the flash-attention order); both differ from the
-// separate path by rounding only.  Pairs are taken longest sequence first (the
-// plan's order), so the largest blocks of work start first.
+// separate path by rounding only.  Items are dealt to the XCDs in runs of
+// kStreamRun consecutive list entries (a sequence's tiles of one head share its
+// K / V rows in that XCD's L2), the runs round-robin.
 // ---------------------------------------------------------------------------
 
 typedef __attribute__((address_space(3))) void lds_void_t;
-typedef __attribute__((ext_vector_type(4))) short short4_t;
-typedef __attribute__((address_space(3))) short4_t lds_short4_t;
 
-#ifndef RAG_STREAM_PER_CU
-#define RAG_STREAM_PER_CU 64
-#endif
-#ifndef RAG_ATTN_TR_ASM
-#define RAG_ATTN_TR_ASM 1
-#endif
-#ifndef RAG_ATTN_STREAM
-#define RAG_ATTN_STREAM 1
-#endif
-#ifndef RAG_ATTN_SNAKE
-#define RAG_ATTN_SNAKE 1
-#endif
-#ifndef RAG_ATTN_WAVES
-#define RAG_ATTN_WAVES 16
-#endif
-constexpr int kAttnWaves = RAG_ATTN_WAVES, kAttnThreads = kAttnWaves * kWave;
-constexpr int kAttnMaxLen = 512;                         // RAG_FUSED_MAX_LEN
-constexpr int kAttnKVElems = kAttnMaxLen * kHeadDim;      // one of K or V in LDS
-constexpr size_t kAttnLds = 2 * kAttnKVElems * sizeof(uint16_t);
-constexpr float kRescaleSlack = 8.f;                      // log2 of the largest exponential kept
+constexpr float kRescaleSlack = 8.f;  // log2 of the largest exponential kept
+constexpr int kStreamWaves = 2, kStreamThreads = kStreamWaves * kWave;
+constexpr int kStreamBlocks = 4 / kStreamWaves;                 // 1 KB copies of K (and of V) per wave and chunk
+constexpr int kStreamChunk = 32;                                // keys per LDS stage
+constexpr int kStreamStageElems = 2 * kStreamChunk * kHeadDim;  // K rows, then V rows
+constexpr int kStreamRun = 8;
+constexpr int kStreamPerCu = 64;  // grid cap in workgroups per CU (they then loop over the list)
+
+__device__ __forceinline__ int stream_item(int bid, int nb) {  // nb: a multiple of 8 * kStreamRun
+    const int xcd = bid % 8, j = bid / 8;
+    return ((j / kStreamRun) * 8 + xcd) * kStreamRun + j % kStreamRun;
+}
 
 // Element offset of (row, col) in [rows][64 channels] LDS storage (128-byte rows,
 // two per 256-byte bank line) whose 16-byte chunks are XOR-swizzled by row bits
@@ -451,191 +442,9 @@ __device__ __forceinline__ float sum_xor32(float v) {
     return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
-// Masked attention: query block qb (32 rows) needs key chunks 0..qb only, so block
-// qb costs qb + 1 chunks.  Waves w and w + 4k share SIMD w % 4; blocks are dealt to
-// waves in a snake (SIMDs 0,1,2,3 then 3,2,1,0, ...) so every SIMD gets the same
-// number of chunks when a sequence has 16 blocks.
-__device__ __forceinline__ int snake_block(int wave) {
-    const int g = wave / 4, s = wave % 4;
-    return 4 * g + ((g & 1) ? 3 - s : s);
-}
-
-template <bool CAUSAL>
-__global__ __launch_bounds__(kAttnThreads) __attribute__((amdgpu_waves_per_eu(kAttnWaves / 4, kAttnWaves / 4)))
-void k_attention_bf16(PlanArgs pa, const int32_t* __restrict__ order, const uint16_t* __restrict__ q, int ldq,
-                      const uint16_t* __restrict__ k, int ldk, const uint16_t* __restrict__ v, int ldv, float scale,
-                      uint16_t* __restrict__ O, int ldo) {
-    if (pa.status[0] != 0) return;
-    extern __shared__ __attribute__((aligned(16))) uint16_t kvs[];  // K rows, then V rows
-    const int H = pa.heads;
-    const int n_pairs = pa.batch * H;
-    const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
-    const int l32 = lane % 32, h2 = lane / 32;
-    // transposed-read addressing inside a 16-lane group (see the header comment)
-    const int tr_e = (lane % 16) / 4, tr_q = lane % 4, tr_g = lane / 16;
-    // z = s * scale * log2(e) with a non-negative factor: a negative scale flips the sign of q instead
-    const float zs = fabsf(scale) * 1.4426950408889634f;
-    const uint32_t qsign = scale < 0.f ? 0x80008000u : 0u;
-
-    for (int round = 0; round * (int)gridDim.x < n_pairs; ++round) {
-#if RAG_ATTN_SNAKE
-        // pairs are dealt in a snake (workgroups 0..G-1, then G-1..0, ...): with the
-        // list longest first, every workgroup's sum of pair costs is then about equal
-        const int pair = round * gridDim.x + ((round & 1) ? gridDim.x - 1 - blockIdx.x : blockIdx.x);
-#else
-        const int pair = round * gridDim.x + blockIdx.x;
-#endif
-        if (pair >= n_pairs) continue;
-        const int b = order[pair / H], h = pair % H;
-        const int L = pa.lengths[b];
-        if (L == 0) continue;
-        const int t0 = pa.tok_off[b];
-        const __amdgpu_buffer_rsrc_t rk = __builtin_amdgcn_make_buffer_rsrc(
-            const_cast<uint16_t*>(k + (int64_t)t0 * ldk + h * kHeadDim), 0, (uint32_t)L * ldk * 2u, 0x00020000);
-        const __amdgpu_buffer_rsrc_t rv = __builtin_amdgcn_make_buffer_rsrc(
-            const_cast<uint16_t*>(v + (int64_t)t0 * ldv + h * kHeadDim), 0, (uint32_t)L * ldv * 2u, 0x00020000);
-        const int rows = (L + 31) & ~31;  // whole 32-key chunks; rows past L arrive as zeros
-        attn_barrier();                  // the previous pair is done with the LDS rows
-        // a wave copy fills one 1 KB block = 8 rows: lane -> row 8*blk + lane/8, physical chunk lane%8
-        for (int blk = wave; blk < rows / 8; blk += kAttnWaves) {
-            const int row = blk * 8 + lane / 8;
-            const int logical = (lane % 8) ^ kv_swz(row);
-            __builtin_amdgcn_raw_ptr_buffer_load_lds(rk, (lds_void_t*)(kvs + blk * 512), 16, row * ldk * 2 + logical * 16, 0, 0, 0);
-            __builtin_amdgcn_raw_ptr_buffer_load_lds(rv, (lds_void_t*)(kvs + kAttnKVElems + blk * 512), 16,
-                                                     row * ldv * 2 + logical * 16, 0, 0, 0);
-        }
-        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-        attn_barrier();
-        const uint16_t* ks_ = kvs;
-        const uint16_t* vs_ = kvs + kAttnKVElems;
-        const int nc = rows / 32;  // key chunks
-        // 32*c and 16*t leave row bits 1-3 (the swizzle's) unchanged, so the LDS
-        // offsets of chunk c are those of chunk 0 plus 32*c rows.
-        int koff[4], voff[2][2];
-#pragma unroll
-        for (int ks = 0; ks < 4; ++ks) koff[ks] = kv_off(l32, 16 * ks + 8 * h2);
-#pragma unroll
-        for (int cb = 0; cb < 2; ++cb)
-#pragma unroll
-            for (int hi = 0; hi < 2; ++hi)
-                voff[cb][hi] = kv_off(4 * (tr_g >> 1) + tr_e + 8 * hi, 32 * cb + 16 * (tr_g & 1) + 4 * tr_q);
-        for (int qb = CAUSAL ? snake_block(wave) : wave; qb * 32 < L; qb += kAttnWaves) {
-            const int qi = min(qb * 32 + l32, L - 1);
-            const int n_chunks = CAUSAL ? qb + 1 : nc;  // masked: keys up to the block's last query
-            const uint16_t* qrow = q + (int64_t)(t0 + qi) * ldq + h * kHeadDim + 8 * h2;
-            bf16x8 qf[4];
-#pragma unroll
-            for (int ks = 0; ks < 4; ++ks) {
-                u32x4 raw = ld16(qrow + 16 * ks);
-                raw ^= qsign;
-                qf[ks] = as_bf16x8(raw);
-            }
-            float m = -INFINITY, lsum = 0.f;
-            floatx16 oacc[2];  // O^T, channels 0-31 and 32-63
-#pragma unroll
-            for (int cb = 0; cb < 2; ++cb)
-#pragma unroll
-                for (int r = 0; r < 16; ++r) oacc[cb][r] = 0.f;
-            // per-lane LDS pointers of chunk 0, advanced by 32 rows per chunk
-            const uint16_t* kp = ks_ + koff[0];
-            const uint16_t* vp = vs_;
-            for (int c = 0; c < n_chunks; ++c, kp += 32 * kHeadDim, vp += 32 * kHeadDim) {
-                floatx16 acc;
-#pragma unroll
-                for (int r = 0; r < 16; ++r) acc[r] = 0.f;
-                bf16x8 kf[4];
-#pragma unroll
-                for (int ks = 0; ks < 4; ++ks)
-                    kf[ks] = as_bf16x8(*reinterpret_cast<const u32x4*>(kp + (koff[ks] - koff[0])));
-                __builtin_amdgcn_sched_barrier(0);  // all four reads in flight before the first MFMA waits
-#pragma unroll
-                for (int ks = 0; ks < 4; ++ks) acc = mfma32x32x16(kf[ks], qf[ks], acc);
-                // keys past the sequence (and, masked, keys after the query) take no part;
-                // the branch is wave-uniform
-                if (32 * (c + 1) > L || (CAUSAL && c == qb)) {
-                    const int kmax = CAUSAL && c == qb ? min(L - 1, qb * 32 + l32) : L - 1;
-#pragma unroll
-                    for (int r = 0; r < 16; ++r)
-                        if (32 * c + 8 * (r / 4) + 4 * h2 + (r % 4) > kmax) acc[r] = -INFINITY;
-                }
-                float cmax = acc[0];
-#pragma unroll
-                for (int r = 1; r < 16; ++r) cmax = fmaxf(cmax, acc[r]);
-                const float cz = max_xor32(cmax) * zs;
-                const bool raise = cz > m + kRescaleSlack;
-                if (__ballot(raise) != 0) {  // rare after the first chunk
-                    const float mn = raise ? cz : m;
-                    const float alpha = raise ? __builtin_amdgcn_exp2f(m - mn) : 1.f;  // 0 on the first chunk
-                    lsum *= alpha;
-#pragma unroll
-                    for (int cb = 0; cb < 2; ++cb)
-#pragma unroll
-                        for (int r = 0; r < 16; ++r) oacc[cb][r] *= alpha;
-                    m = mn;
-                }
-#pragma unroll
-                for (int t = 0; t < 2; ++t) {  // 16-key steps
-                    u32x4 pw;
-#pragma unroll
-                    for (int e = 0; e < 4; ++e) {
-                        const float e0 = __builtin_amdgcn_exp2f(fmaf(acc[8 * t + 2 * e], zs, -m));
-                        const float e1 = __builtin_amdgcn_exp2f(fmaf(acc[8 * t + 2 * e + 1], zs, -m));
-                        lsum += e0 + e1;
-                        pw[e] = pack_bf16x2(e0, e1);
-                    }
-                    const bf16x8 pb = as_bf16x8(pw);
-#pragma unroll
-                    for (int cb = 0; cb < 2; ++cb) {
-                        const uint16_t* vt = vp + 16 * t * kHeadDim;
-                        const short4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_short4_t*)(vt + voff[cb][0]));
-                        const short4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_short4_t*)(vt + voff[cb][1]));
-                        const u32x4 va = {(uint32_t)(uint16_t)lo[0] | ((uint32_t)(uint16_t)lo[1] << 16),
-                                          (uint32_t)(uint16_t)lo[2] | ((uint32_t)(uint16_t)lo[3] << 16),
-                                          (uint32_t)(uint16_t)hi[0] | ((uint32_t)(uint16_t)hi[1] << 16),
-                                          (uint32_t)(uint16_t)hi[2] | ((uint32_t)(uint16_t)hi[3] << 16)};
-                        oacc[cb] = mfma32x32x16(as_bf16x8(va), pb, oacc[cb]);
-                    }
-                }
-            }
-            const float inv = 1.0f / sum_xor32(lsum);
-            // O^T accumulator: lane holds channels 32*cb + 8*(r/4) + 4*h2 + r%4 of query l32
-            const int i = qb * 32 + l32;
-            if (i < L) {
-                uint16_t* orow = O + (int64_t)(t0 + i) * ldo + h * kHeadDim;
-#pragma unroll
-                for (int cb = 0; cb < 2; ++cb)
-#pragma unroll
-                    for (int g = 0; g < 4; ++g) {
-                        const u32x2 w2 = {pack_bf16x2(oacc[cb][4 * g] * inv, oacc[cb][4 * g + 1] * inv),
-                                          pack_bf16x2(oacc[cb][4 * g + 2] * inv, oacc[cb][4 * g + 3] * inv)};
-                        *reinterpret_cast<u32x2*>(orow + 32 * cb + 8 * g + 4 * h2) = w2;
-                    }
-            }
-        }
-    }
-}
-
-// Streaming variant: one (sequence b, head h, 64-query tile) item of the plan's
-// Attn.V list per workgroup of two waves (32 queries each).  The keys stream
-// through two LDS stages of 32 K rows and 32 V rows (16 KB per workgroup), so
-// eight workgroups share a CU: while one waits for its next chunk, the others
-// compute, and every SIMD keeps four busy waves whatever the sequence lengths.
-// The per-chunk arithmetic is the pair kernel's above.  Items are dealt to the
-// XCDs in runs of kStreamRun consecutive list entries (a sequence's tiles of one
-// head share its K / V rows in that XCD's L2), the runs round-robin.
-constexpr int kStreamWaves = 2, kStreamThreads = kStreamWaves * kWave;
-constexpr int kStreamChunk = 32;                                // keys per LDS stage
-constexpr int kStreamStageElems = 2 * kStreamChunk * kHeadDim;  // K rows, then V rows
-constexpr int kStreamRun = 8;
-
-__device__ __forceinline__ int stream_item(int bid, int nb) {  // nb: a multiple of 8 * kStreamRun
-    const int xcd = bid % 8, j = bid / 8;
-    return ((j / kStreamRun) * 8 + xcd) * kStreamRun + j % kStreamRun;
-}
-
 template <bool CAUSAL>
 __global__ __launch_bounds__(kStreamThreads) __attribute__((amdgpu_waves_per_eu(4)))
-void k_attention_stream_bf16(PlanArgs pa, const uint16_t* __restrict__ q, int ldq, const uint16_t* __restrict__ k,
+void k_attention_bf16(PlanArgs pa, const uint16_t* __restrict__ q, int ldq, const uint16_t* __restrict__ k,
                              int ldk, const uint16_t* __restrict__ v, int ldv, float scale,
                              uint16_t* __restrict__ O, int ldo) {
     if (pa.status[0] != 0) return;
@@ -673,7 +482,7 @@ void k_attention_stream_bf16(PlanArgs pa, const uint16_t* __restrict__ q, int ld
         const int qb = 2 * ti + wave;  // this wave's 32-query block
         const bool active = qb * 32 < L;
         const int nc_all = (L + 31) / 32;
-        const int nc_wg = CAUSAL ? min(nc_all, 2 * ti + 2) : nc_all;  // chunks the workgroup loads
+        const int nc_wg = CAUSAL ? min(nc_all, 2 * ti + kStreamWaves) : nc_all;  // chunks the workgroup loads
         const int nc_me = CAUSAL ? qb + 1 : nc_all;                    // chunks this wave uses
         const __amdgpu_buffer_rsrc_t rk = __builtin_amdgcn_make_buffer_rsrc(
             const_cast<uint16_t*>(k + (int64_t)t0 * ldk + h * kHeadDim), 0, (uint32_t)L * ldk * 2u, 0x00020000);
@@ -682,10 +491,10 @@ void k_attention_stream_bf16(PlanArgs pa, const uint16_t* __restrict__ q, int ld
         // wave w copies rows 16w .. 16w + 15 of the chunk's K and V (two 1 KB blocks
         // of 8 rows each); rows past L arrive as zeros.  Chunk c adds 32c rows to
         // the lane offsets of chunk 0 (32c leaves the swizzle's row bits alone).
-        int vko[2], vvo[2];
+        int vko[kStreamBlocks], vvo[kStreamBlocks];
 #pragma unroll
-        for (int i = 0; i < 2; ++i) {
-            const int row = (wave * 2 + i) * 8 + lane / 8;
+        for (int i = 0; i < kStreamBlocks; ++i) {
+            const int row = (wave * kStreamBlocks + i) * 8 + lane / 8;
             const int logical = (lane % 8) ^ kv_swz(row);
             vko[i] = row * ldk * 2 + logical * 16;
             vvo[i] = row * ldv * 2 + logical * 16;
@@ -694,8 +503,8 @@ void k_attention_stream_bf16(PlanArgs pa, const uint16_t* __restrict__ q, int ld
             uint16_t* st = kvs + decltype(stg)::value * kStreamStageElems;
             const int dk = c * kStreamChunk * ldk * 2, dv = c * kStreamChunk * ldv * 2;
 #pragma unroll
-            for (int i = 0; i < 2; ++i) {
-                const int blk = wave * 2 + i;
+            for (int i = 0; i < kStreamBlocks; ++i) {
+                const int blk = wave * kStreamBlocks + i;
                 __builtin_amdgcn_raw_ptr_buffer_load_lds(rk, (lds_void_t*)(st + blk * 512), 16, vko[i] + dk, 0, 0, 0);
                 __builtin_amdgcn_raw_ptr_buffer_load_lds(rv, (lds_void_t*)(st + kStreamChunk * kHeadDim + blk * 512),
                                                          16, vvo[i] + dv, 0, 0, 0);
@@ -865,31 +674,14 @@ namespace {
 template <bool CAUSAL>
 hipError_t launch_fused_variant(const PlanView& p, const void* q, int ldq, const void* k, int ldk, const void* v,
                                 int ldv, float scale, void* out, int ldo, hipStream_t s) {
-    static bool attr_set = false;  // benign race: every thread sets the same value
-    if (!attr_set) {
-        hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_attention_bf16<CAUSAL>),
-                                           hipFuncAttributeMaxDynamicSharedMemorySize, (int)kAttnLds);
-        if (e != hipSuccess) return e;
-        attr_set = true;
-    }
-    const PlanArgs pa = plan_args(p);
-#if RAG_ATTN_STREAM
-    {
-        // one workgroup per item, at most 64 per CU (the workgroups then loop over
-        // the list); a multiple of 8 * kStreamRun so the XCD dealing is a permutation
-        constexpr int64_t kUnit = 8 * kStreamRun;
-        const int64_t cap = std::max<int64_t>(p.av_cap, 1);
-        const int64_t limit = (int64_t)device_cu_count() * RAG_STREAM_PER_CU;
-        const int64_t g = (std::min(cap, limit) + kUnit - 1) / kUnit * kUnit;
-        hipLaunchKernelGGL(k_attention_stream_bf16<CAUSAL>, dim3((unsigned)g), dim3(kStreamThreads), 0, s, pa,
-                           static_cast<const uint16_t*>(q), ldq, static_cast<const uint16_t*>(k), ldk,
-                           static_cast<const uint16_t*>(v), ldv, scale, static_cast<uint16_t*>(out), ldo);
-        return hipGetLastError();
-    }
-#endif
-    const int64_t pairs = (int64_t)p.batch * p.heads;
-    const int grid = static_cast<int>(std::min<int64_t>(pairs, device_cu_count()));
-    hipLaunchKernelGGL(k_attention_bf16<CAUSAL>, dim3(grid), dim3(kAttnThreads), kAttnLds, s, pa, p.order,
+    // one workgroup per item, at most kStreamPerCu per CU (the workgroups then
+    // loop over the list); a multiple of 8 * kStreamRun so the XCD dealing is a
+    // permutation
+    constexpr int64_t kUnit = 8 * kStreamRun;
+    const int64_t cap = std::max<int64_t>(p.av_cap, 1);
+    const int64_t limit = (int64_t)device_cu_count() * kStreamPerCu;
+    const int64_t g = (std::min(cap, limit) + kUnit - 1) / kUnit * kUnit;
+    hipLaunchKernelGGL(k_attention_bf16<CAUSAL>, dim3((unsigned)g), dim3(kStreamThreads), 0, s, plan_args(p),
                        static_cast<const uint16_t*>(q), ldq, static_cast<const uint16_t*>(k), ldk,
                        static_cast<const uint16_t*>(v), ldv, scale, static_cast<uint16_t*>(out), ldo);
     return hipGetLastError();
@@ -899,7 +691,7 @@ hipError_t launch_fused_variant(const PlanView& p, const void* q, int ldq, const
 hipError_t launch_fused_attention(const PlanView& p, int dtype, const void* q, int ldq, const void* k, int ldk,
                                   const void* v, int ldv, float scale, void* out, int ldo, bool causal,
                                   hipStream_t s) {
-    if (dtype != 1 || p.max_len > kAttnMaxLen) return hipErrorInvalidValue;
+    if (dtype != 1) return hipErrorInvalidValue;
     return causal ? launch_fused_variant<true>(p, q, ldq, k, ldk, v, ldv, scale, out, ldo, s)
                   : launch_fused_variant<false>(p, q, ldq, k, ldk, v, ldv, scale, out, ldo, s);
 }

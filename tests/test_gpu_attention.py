@@ -143,21 +143,14 @@ def _fused(L, H, q, k, v, scale):
     return host(O, "bf16").reshape(T, d)
 
 
-@pytest.mark.parametrize("L", RAGGED + [[512] * 3, [8, 64, 9, 384, 511]])
+@pytest.mark.parametrize("L", RAGGED + [[512] * 3, [8, 64, 9, 384, 511], [700, 1030, 3, 64, 0, 1537]])
 @pytest.mark.parametrize("H", [1, 4])
 @pytest.mark.parametrize("qk_scale", [0.5, 4.0])
 def test_fused_attention(L, H, qk_scale):
     rng = np.random.default_rng(sum(L) + H)
     L = np.array(L, np.int32)
     T = int(L.sum())
-    if L.max() > 512:  # beyond the fused kernel's register-resident rows: rejected on the host
-        import paper_2110_10221_amd as rag
-
-        plan = _plan(L, H)
-        z = torch.zeros(T, H * 64, dtype=torch.bfloat16, device="cuda")
-        with pytest.raises(rag.RaggedError, match="RAG_ERR_SHAPE"):
-            rag.ragged_attention(plan, z, z, z, torch.empty_like(z), 0.125)
-        return
+    print(f"fused L={L.tolist()} H={H} qk_scale={qk_scale}", flush=True)
     q, k = (random_storage(rng, (T, H * 64), "bf16", qk_scale) for _ in range(2))
     v = random_storage(rng, (T, H * 64), "bf16", 1.0)
     got = _fused(L, H, q, k, v, 1 / 8)
@@ -216,6 +209,18 @@ def test_fused_attention_sdpa_workload():
     L, H = wl.lengths, wl.cfg.heads
     got = _fused(L, H, wl.tensors["q"], wl.tensors["k"], wl.tensors["v"], 0.125)
     _fused_close(got, L, H, wl.tensors["q"], wl.tensors["k"], wl.tensors["v"], 0.125)
+
+
+def test_fused_attention_rejects_rows_beyond_32bit_offsets():
+    # max_len * ld * 2 bytes must stay below 2^31: a plan promising 2^24-token rows
+    # of leading dimension 64 is refused on the host before anything launches
+    import paper_2110_10221_amd as rag
+
+    L, H = np.array([3, 5], np.int32), 1
+    plan = rag.Plan(torch.from_numpy(L).cuda(), int(L.sum()), 1 << 24, H)
+    z = torch.zeros(int(L.sum()), 64, dtype=torch.bfloat16, device="cuda")
+    with pytest.raises(rag.RaggedError, match="RAG_ERR_SHAPE"):
+        rag.ragged_attention(plan, z, z, z, torch.empty_like(z), 0.125)
 
 
 def test_fused_attention_negative_scale():

@@ -47,7 +47,7 @@ def _small_weights(rng, d, dff, dtype):
 
 
 @pytest.mark.parametrize("dtype,flags", [("bf16", 0), ("bf16", 1), ("f32", 0)])
-@pytest.mark.parametrize("L", [[5, 70, 33], [1], [0, 64, 0, 129], [200, 17, 64, 3, 99]])
+@pytest.mark.parametrize("L", [[5, 70, 33], [1], [0, 64, 0, 129], [200, 17, 64, 3, 99], [700, 40, 3]])
 def test_small_layers(dtype, flags, L):
     rng = np.random.default_rng(sum(L))
     L = np.array(L, np.int32)

@@ -174,14 +174,15 @@ def test_fused_causal_first_rows_and_prefix():
     assert np.array_equal(got_m, got[idx])
 
 
-def test_fused_causal_rejects_long_rows():
-    import paper_2110_10221_amd as rag
-
-    L, H = np.array([600, 3], np.int32), 1
-    plan = _plan(L, H)
-    z = torch.zeros(int(L.sum()), 64, dtype=torch.bfloat16, device="cuda")
-    with pytest.raises(rag.RaggedError, match="RAG_ERR_SHAPE"):
-        rag.ragged_attention_causal(plan, z, z, z, torch.empty_like(z), 0.125)
+@pytest.mark.parametrize("L", [[600, 3], [1100, 0, 77, 513]])
+def test_fused_causal_long_rows(L):
+    # rows longer than 512 keys stream through the same LDS stages
+    rng = np.random.default_rng(sum(L))
+    L, H = np.array(L, np.int32), 2
+    T = int(L.sum())
+    print(f"fused causal long L={L.tolist()}", flush=True)
+    q, k, v = (random_storage(rng, (T, H * 64), "bf16", 1.0) for _ in range(3))
+    _fused_causal_close(_fused_causal(L, H, q, k, v, 0.125), L, H, q, k, v, 0.125)
 
 
 @pytest.mark.parametrize("dtype,flags", [("bf16", 2), ("bf16", 3), ("f32", 2)])
