@@ -1,17 +1,21 @@
-// Ragged scaled dot-product attention as three operators over the plan's work
-// lists (the paper's QK^T, Softmax and AttnV operators):
-//   ragged QK^T     one workgroup item = one 64x64 score tile of one sequence and
-//                   head; the tile never crosses a sequence boundary, so no
-//                   padded work is done beyond the predicated edge tile
+// Ragged scaled dot-product attention over the plan's work lists: the paper's
+// QK^T, Softmax and AttnV operators one by one, and the three fused.
+//   ragged QK^T     bf16: one workgroup item = one (sequence, head, 64-query
+//                   block), walking every 64-key tile of its rows; fp32: one
+//                   item = one 64x64 score tile.  No tile crosses a sequence
+//                   boundary, so no padded work is done beyond predicated edges
 //   ragged softmax  one wave per token: the token's H rows (each L_b scores)
 //                   are contiguous in the X[b][i][h][j] layout
 //   ragged Attn.V   one workgroup item = 64 query rows of one sequence and head,
 //                   reducing over that sequence's L_b keys
-// Persistent grids walk the lists in order: sequences longest first.
+//   fused           one (sequence, head, 64-query tile) item per two-wave
+//                   workgroup, keys streamed through LDS (details further down)
+// The operators' persistent grids walk the lists in order: sequences longest first.
 //
-// bf16 kernels use v_mfma_f32_16x16x32_bf16.  In a 16x16x32 MFMA lane l supplies
-// row (l % 16) of A and column (l % 16) of B, each with the 8 consecutive k values
-// 8*(l/16) .. 8*(l/16)+7, and receives C rows 4*(l/16) .. 4*(l/16)+3 of column l % 16.
+// The unfused bf16 kernels use v_mfma_f32_16x16x32_bf16.  In a 16x16x32 MFMA lane l
+// supplies row (l % 16) of A and column (l % 16) of B, each with the 8 consecutive
+// k values 8*(l/16) .. 8*(l/16)+7, and receives C rows 4*(l/16) .. 4*(l/16)+3 of
+// column l % 16.
 #include <algorithm>
 #include <cfloat>
 
