@@ -372,8 +372,11 @@ rag_status ragged_trmm(const void* l, int32_t ldl, const void* b, int32_t ldb, v
 enum {
     RAG_LAYER_UNFUSED_ATTENTION = 1, /* run ragged_qkt/softmax/attn_v with a
                                         materialised score buffer in the workspace */
-    RAG_LAYER_CAUSAL = 2             /* masked attention (position i sees keys j <= i):
+    RAG_LAYER_CAUSAL = 2,            /* masked attention (position i sees keys j <= i):
                                         the decoder variant of the layer */
+    RAG_LAYER_BUILD_PLAN = 4         /* build the plan first, exactly as ragged_offsets()
+                                        would (bf16 batches of up to 256 sequences: inside
+                                        the QKV projection's launch, which does not read it) */
 };
 
 /* Number of events encoder_layer records when `events` is not NULL. */
@@ -394,8 +397,10 @@ rag_status encoder_layer_workspace(int32_t total_tokens, int32_t max_len, int32_
  * (the paper's nine-operator layer, Section 7.2 and Appendix D):
  *   QKV = x Wqkv^T + bqkv;  P = softmax(Q K^T / sqrt(dh)) per sequence and head;
  *   O = P V;  H1 = LN1(O Wo^T + bo + x);  y = LN2(act(H1 W1^T + b1) W2^T + b2 + H1)
- * `plan` must have been built by ragged_offsets() for the batch (it is only
- * read).  x, y are [T, d_model] contiguous and must not overlap.  `events`, if
+ * `plan` must have been built by ragged_offsets() for the batch (it is then
+ * only read), unless `flags` holds RAG_LAYER_BUILD_PLAN: the layer then fills
+ * the plan's arrays itself before its attention stage, with the same results
+ * and data-error reporting as ragged_offsets().  x, y are [T, d_model] contiguous and must not overlap.  `events`, if
  * not NULL, holds RAG_LAYER_EVENTS hipEvent_t handles created by the caller:
  * events[k] is recorded on `stream` before stage k and events[9] after stage
  * 8, with the stages 0 QKV projection, 1 QK^T, 2 softmax, 3 Attn.V, 4 output

@@ -27,6 +27,7 @@ RAG_TILE = 64
 RAG_HEAD_DIM = 64
 RAG_LAYER_UNFUSED_ATTENTION = 1
 RAG_LAYER_CAUSAL = 2
+RAG_LAYER_BUILD_PLAN = 4
 RAG_LAYER_EVENTS = 10
 DATA_BITS = {1: "negative length", 2: "length > max_len", 4: "sum of lengths != total_tokens",
              8: "qkt_cap exceeded", 16: "av_cap exceeded", 32: "score buffer too small"}

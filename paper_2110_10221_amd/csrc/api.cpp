@@ -413,7 +413,8 @@ rag_status encoder_layer(const rag_plan* plan, const void* x, void* y, int32_t d
     if (heads != plan->heads) return fail(RAG_ERR_SHAPE, "%s: heads %d differs from the plan's %d", fn, heads, plan->heads);
     if (head_dim != RAG_HEAD_DIM) return fail(RAG_ERR_SHAPE, "%s: head_dim %d unsupported (only %d)", fn, head_dim, RAG_HEAD_DIM);
     if (d_model != heads * head_dim) return fail(RAG_ERR_SHAPE, "%s: d_model %d != heads * head_dim", fn, d_model);
-    if (flags & ~(RAG_LAYER_UNFUSED_ATTENTION | RAG_LAYER_CAUSAL)) return fail(RAG_ERR_ARG, "%s: unknown flags 0x%x", fn, flags);
+    if (flags & ~(RAG_LAYER_UNFUSED_ATTENTION | RAG_LAYER_CAUSAL | RAG_LAYER_BUILD_PLAN))
+        return fail(RAG_ERR_ARG, "%s: unknown flags 0x%x", fn, flags);
     const int T = plan->total_tokens, d = d_model;
     const LayerBuffers lb = layer_buffers(T, plan->max_len, d, heads, d_ff, dtype, flags);
     if (!workspace || workspace_bytes < lb.total)
@@ -451,7 +452,8 @@ rag_status encoder_layer(const rag_plan* plan, const void* x, void* y, int32_t d
     const float scale = 1.0f / sqrtf((float)head_dim);
     const bool causal = (flags & RAG_LAYER_CAUSAL) != 0;
     mark(0);
-    run(rag::launch_linear(dtype, x, d, w->w_qkv, w->b_qkv, nullptr, 0, RAG_ACT_NONE, qkv, 3 * d, T, d, 3 * d, s));
+    run(rag::launch_linear(dtype, x, d, w->w_qkv, w->b_qkv, nullptr, 0, RAG_ACT_NONE, qkv, 3 * d, T, d, 3 * d, s,
+                           (flags & RAG_LAYER_BUILD_PLAN) ? &v : nullptr));
     mark(1);
     if (unfused_attention(dtype, flags, plan->max_len, d)) {
         const int64_t cap = (int64_t)(lb.scores / es);

@@ -44,6 +44,7 @@
 
 #include "device_common.h"
 #include "launch.h"
+#include "plan_device.h"
 
 namespace rag {
 namespace {
@@ -536,12 +537,21 @@ __device__ __forceinline__ void gemm_tile_bf16(const uint16_t* __restrict__ x, i
 // XCD-aware order; when the last round of tiles would fill at most half the
 // workgroup slots (two per CU), its tiles instead run as two 64-token halves
 // each, workgroups n_full onwards, so that round takes about half a tile's time.
+// Workgroups from n_gemm on (if any) build a batch's plan instead: the layer's
+// QKV projection carries the prelude that way, in the slots its last round of
+// tiles leaves free.
+static_assert(sizeof(PlanSmem) <= tile_lds_bytes<64, false>(), "the plan's LDS fits the GEMM's");
+
 template <int ACT, bool HAS_BIAS, bool HAS_RES>
 __global__ __launch_bounds__(Cfg<128>::kThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void k_gemm_bf16(const uint16_t* __restrict__ x, int ldx, const uint16_t* __restrict__ w,
                  const uint16_t* __restrict__ bias, const uint16_t* residual, int ldr, uint16_t* y, int ldy,
-                 int T, int K, int N, int tiles_m, int tiles_n, int n_full) {
+                 int T, int K, int N, int tiles_m, int tiles_n, int n_full, int n_gemm, PlanFillArgs pf) {
     extern __shared__ __attribute__((aligned(16))) uint16_t smem[];
+    if ((int)blockIdx.x >= n_gemm) {
+        plan_fused_body(pf, blockIdx.x - n_gemm, *reinterpret_cast<PlanSmem*>(smem));
+        return;
+    }
     int tm, tn;
     if ((int)blockIdx.x < n_full) {
         tile_coords(blockIdx.x, n_full, tiles_m, tiles_n, tm, tn);
@@ -811,7 +821,7 @@ __global__ __launch_bounds__(256) void k_trmm_f32(const float* __restrict__ l, i
 
 template <int ACT, bool HB, bool HR>
 hipError_t launch_bf16_tiles(const void* x, int ldx, const void* w, const void* bias, const void* residual, int ldr,
-                             void* y, int ldy, int T, int K, int N, hipStream_t s) {
+                             void* y, int ldy, int T, int K, int N, const PlanView* plan, hipStream_t s) {
     constexpr int kLds = tile_lds_bytes<128, false>() > tile_lds_bytes<64, false>() ? tile_lds_bytes<128, false>()
                                                                                     : tile_lds_bytes<64, false>();
     const int tiles_m = (T + 127) / 128, tiles_n = (N + BN - 1) / BN, tiles = tiles_m * tiles_n;
@@ -825,21 +835,23 @@ hipError_t launch_bf16_tiles(const void* x, int ldx, const void* w, const void* 
         if (e != hipSuccess) return e;
         attr_set = true;
     }
-    hipLaunchKernelGGL((k_gemm_bf16<ACT, HB, HR>), dim3(n_full + 2 * (tiles - n_full)), dim3(Cfg<128>::kThreads),
+    const int n_gemm = n_full + 2 * (tiles - n_full);
+    const PlanFillArgs pf = plan ? plan_fill_args(*plan) : PlanFillArgs{};
+    hipLaunchKernelGGL((k_gemm_bf16<ACT, HB, HR>), dim3(n_gemm + (plan ? plan->batch : 0)), dim3(Cfg<128>::kThreads),
                        kLds, s, static_cast<const uint16_t*>(x), ldx, static_cast<const uint16_t*>(w),
                        static_cast<const uint16_t*>(bias), static_cast<const uint16_t*>(residual), ldr,
-                       static_cast<uint16_t*>(y), ldy, T, K, N, tiles_m, tiles_n, n_full);
+                       static_cast<uint16_t*>(y), ldy, T, K, N, tiles_m, tiles_n, n_full, n_gemm, pf);
     return hipGetLastError();
 }
 
 template <int ACT>
 hipError_t launch_bf16_act(const void* x, int ldx, const void* w, const void* bias, const void* residual, int ldr,
-                           void* y, int ldy, int T, int K, int N, hipStream_t s) {
+                           void* y, int ldy, int T, int K, int N, const PlanView* plan, hipStream_t s) {
     auto* f = &launch_bf16_tiles<ACT, false, false>;
     if (bias && residual) f = &launch_bf16_tiles<ACT, true, true>;
     else if (bias) f = &launch_bf16_tiles<ACT, true, false>;
     else if (residual) f = &launch_bf16_tiles<ACT, false, true>;
-    return f(x, ldx, w, bias, residual, ldr, y, ldy, T, K, N, s);
+    return f(x, ldx, w, bias, residual, ldr, y, ldy, T, K, N, plan, s);
 }
 
 }  // namespace
@@ -897,12 +909,19 @@ hipError_t launch_trmm(int dtype, const void* l, int ldl, const void* b, int ldb
 }
 
 hipError_t launch_linear(int dtype, const void* x, int ldx, const void* w, const void* bias, const void* residual,
-                         int ldr, int act, void* y, int ldy, int T, int K, int N, hipStream_t s) {
+                         int ldr, int act, void* y, int ldy, int T, int K, int N, hipStream_t s,
+                         const PlanView* plan) {
+    if (plan && (dtype != 1 || T == 0 || plan->batch > kFusedBatch)) {
+        // the plan rides along only with a bf16 projection; otherwise its own launch goes first
+        const hipError_t e = launch_offsets(*plan, s);
+        if (e != hipSuccess) return e;
+        plan = nullptr;
+    }
     if (T == 0) return hipSuccess;
     if (dtype == 1) {
-        if (act == 1) return launch_bf16_act<1>(x, ldx, w, bias, residual, ldr, y, ldy, T, K, N, s);
-        if (act == 2) return launch_bf16_act<2>(x, ldx, w, bias, residual, ldr, y, ldy, T, K, N, s);
-        return launch_bf16_act<0>(x, ldx, w, bias, residual, ldr, y, ldy, T, K, N, s);
+        if (act == 1) return launch_bf16_act<1>(x, ldx, w, bias, residual, ldr, y, ldy, T, K, N, plan, s);
+        if (act == 2) return launch_bf16_act<2>(x, ldx, w, bias, residual, ldr, y, ldy, T, K, N, plan, s);
+        return launch_bf16_act<0>(x, ldx, w, bias, residual, ldr, y, ldy, T, K, N, plan, s);
     }
     const dim3 grid((T + 63) / 64, (N + 63) / 64);
     const float* xf = static_cast<const float*>(x);

@@ -41,9 +41,12 @@ hipError_t launch_fused_attention(const PlanView& p, int dtype, const void* q, i
                                   int ldk, const void* v, int ldv, float scale, void* out, int ldo,
                                   bool causal, hipStream_t s);
 
+// With `plan`, the launch also builds that batch's plan (as launch_offsets does):
+// bf16 projections of batches up to 256 sequences carry the prelude's
+// workgroups behind their tiles, other cases launch the prelude first.
 hipError_t launch_linear(int dtype, const void* x, int ldx, const void* w, const void* bias,
                          const void* residual, int ldr, int act, void* y, int ldy, int T, int K, int N,
-                         hipStream_t s);
+                         hipStream_t s, const PlanView* plan = nullptr);
 
 // Variable-sized batched GEMM.  VgemmView mirrors rag_vgemm_plan.
 struct VgemmView {

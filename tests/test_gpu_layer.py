@@ -108,3 +108,72 @@ def test_layer_permutation_equivariance_and_determinism():
     cat = lambda arr: np.concatenate([arr[st[i]:st[i + 1]] for i in perm])
     c = _gpu_layer(L[perm], cat(wl.tensors["x"]), w, cfg.d_model, cfg.heads, cfg.d_ff, "bf16")
     assert (c == cat(a)).all()
+
+
+def _plan_arrays(plan, n_qkt, n_av):
+    return {"tok_off": plan.tok_off.cpu().numpy(), "att_off": plan.att_off.cpu().numpy(),
+            "order": plan.order.cpu().numpy(), "tok_seq": plan.tok_seq[:plan.total_tokens].cpu().numpy(),
+            "qkt_item_off": plan.qkt_item_off.cpu().numpy(), "av_item_off": plan.av_item_off.cpu().numpy(),
+            "qkt_items": plan.qkt_items[:4 * n_qkt].cpu().numpy(), "av_items": plan.av_items[:3 * n_av].cpu().numpy(),
+            "status": plan.status.cpu().numpy()}
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("L", [[5, 70, 33, 0, 129], [1] * 256, [3] * 257])
+def test_layer_builds_its_plan(dtype, L):
+    # RAG_LAYER_BUILD_PLAN: the same output bits and plan arrays as ragged_offsets
+    # followed by the layer (bf16 batches up to 256 carry the prelude in the QKV
+    # projection's launch; fp32 and larger batches launch it first)
+    import paper_2110_10221_amd as rag
+
+    rng = np.random.default_rng(len(L))
+    L = np.array(L, np.int32)
+    L[1::7] += 9
+    T, H, d, dff = int(L.sum()), 2, 128, 256
+    w = _small_weights(rng, d, dff, dtype)
+    x = random_storage(rng, (T, d), dtype)
+    print(f"layer building its plan {dtype} B={len(L)} T={T}", flush=True)
+    ref = _gpu_layer(L, x, w, d, H, dff, dtype)
+    lens = torch.from_numpy(L).cuda()
+    ref_plan = rag.Plan(lens, T, int(L.max()), H)
+    rag.ragged_offsets(ref_plan)
+    plan = rag.Plan(lens, T, int(L.max()), H)
+    for a in (plan.tok_off, plan.order, plan.tok_seq, plan.qkt_item_off, plan.av_item_off, plan.qkt_items,
+              plan.av_items):
+        a.fill_(-7)  # anything not written would show
+    plan.att_off.fill_(-7)
+    wd = {n: dev(a, dtype) for n, a in w.items()}
+    code = rag.RAG_F32 if dtype == "f32" else rag.RAG_BF16
+    flags = rag.RAG_LAYER_BUILD_PLAN
+    ws = torch.empty(rag.encoder_layer_workspace(T, int(L.max()), d, H, dff, code, flags), dtype=torch.uint8,
+                     device="cuda")
+    whole, y = canary_buffer(T * d, dtype)
+    rag.encoder_layer(plan, dev(x, dtype), y.view(T, d), wd, dff, ws, flags=flags)
+    torch.cuda.synchronize()
+    assert canary_intact(whole, T * d)
+    assert np.array_equal(host(y, dtype).reshape(T, d), ref)
+    n_qkt, n_av = int(ref_plan.status[1].item()), int(ref_plan.status[2].item())
+    got, want = _plan_arrays(plan, n_qkt, n_av), _plan_arrays(ref_plan, n_qkt, n_av)
+    for k in want:
+        assert np.array_equal(got[k], want[k]), k
+
+
+def test_layer_building_its_plan_reports_data_errors():
+    # a token count that disagrees with the lengths: flagged, and attention writes nothing
+    import paper_2110_10221_amd as rag
+
+    rng = np.random.default_rng(3)
+    L = np.array([5, 70, 33], np.int32)
+    T, H, d, dff = int(L.sum()), 2, 128, 256
+    w = _small_weights(rng, d, dff, "bf16")
+    lens = torch.from_numpy(L).cuda()
+    plan = rag.Plan(lens, T + 1, int(L.max()), H)
+    wd = {n: dev(a, "bf16") for n, a in w.items()}
+    flags = rag.RAG_LAYER_BUILD_PLAN
+    ws = torch.empty(rag.encoder_layer_workspace(T + 1, int(L.max()), d, H, dff, rag.RAG_BF16, flags),
+                     dtype=torch.uint8, device="cuda")
+    x = dev(random_storage(rng, (T + 1, d), "bf16"), "bf16")
+    y = torch.empty(T + 1, d, dtype=torch.bfloat16, device="cuda")
+    rag.encoder_layer(plan, x, y, wd, dff, ws, flags=flags)
+    torch.cuda.synchronize()
+    assert plan.data_errors() and "token" in " ".join(plan.data_errors()).lower(), plan.data_errors()
