@@ -98,15 +98,34 @@ def padded_fraction(L, d, dff):
     return 1.0 - useful_flops(L, d, dff) / useful_flops(Lp, d, dff)
 
 
-COMMON_DEVICE_SOURCE = "paper_2110_10221_amd/csrc/device_common.h"
+CSRC = "paper_2110_10221_amd/csrc"
 
 
 def source_hash(path):
-    """Hash of a kernel's source together with the device header it includes."""
+    """Hash of a kernel's source together with every local header of the
+    library's source folder (any of them may be included by it)."""
     h = hashlib.sha256()
-    for p in (path, COMMON_DEVICE_SOURCE):
+    headers = sorted(f for f in os.listdir(os.path.join(ROOT, CSRC)) if f.endswith(".h"))
+    for p in [path] + [f"{CSRC}/{f}" for f in headers]:
+        h.update(p.encode())
         h.update(open(os.path.join(ROOT, p), "rb").read())
     return h.hexdigest()[:16]
+
+
+def length_text(recipe):
+    """Human-readable length distribution of a workload recipe (workloads.draw_lengths)."""
+    kind, _, rest = recipe.partition(":")
+    v = rest.split(":")
+    if kind == "fixed":
+        return f"lengths {{{rest.replace(',', ', ')}}}"
+    if kind == "uniform":
+        return f"lengths uniform [{v[0]}, {v[1]}]"
+    if kind == "lognormal":
+        return f"lengths lognormal (median {v[0]}, sigma {v[1]}, max {v[2]})"
+    if kind == "skew":
+        return (f"lengths skewed ({round(100 * float(v[4]))}% uniform [{v[2]}, {v[3]}], "
+                f"the rest uniform [{v[0]}, {v[1]}])")
+    return f"lengths {recipe}"
 
 
 def load_traffic(kernel):
@@ -699,7 +718,7 @@ def main():
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic",
-        "config": {"workload": f"ragged encoder layer, batch {cfg.batch}, lengths uniform [32, 512] (seed {args.seed}), "
+        "config": {"workload": f"ragged encoder layer, batch {cfg.batch}, {length_text(cfg.lengths)} (seed {args.seed}), "
                                f"d_model {d}, {H} heads x 64, FFN {dff}, GELU, post-LN",
                    "global_batch": cfg.batch, "total_tokens": T, "max_len": int(L.max()),
                    "parallelism": "single GPU", "attention": "unfused" if args.flags & 1 else "fused"},

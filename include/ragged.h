@@ -327,6 +327,17 @@ typedef struct rag_vgemm_plan {
 rag_status vgemm_plan_capacity(int32_t batch, int32_t max_m, int32_t max_n, int64_t* tile_cap /* (host) out */);
 
 /*
+ * (host only)  The exact number of output tiles of a batch whose sizes the
+ * caller also holds on the host: dims (host) is [batch][3] of (m_b, n_b, k_b),
+ * the same array plan->dims holds on the device, and *tiles receives
+ * sum_b ceil(m_b / RAG_VGEMM_TILE_M) * ceil(n_b / RAG_VGEMM_TILE_N), the
+ * smallest tile_cap that serves the batch.  RAG_ERR_ARG for a NULL pointer, a
+ * batch outside [1, RAG_VGEMM_MAX_BATCH] or a size outside [0,
+ * RAG_VGEMM_MAX_DIM].  Launches nothing.
+ */
+rag_status vgemm_tile_count(int32_t batch, const int32_t* dims /* (host) */, int64_t* tiles /* (host) out */);
+
+/*
  * Build the vgemm plan's device arrays from plan->dims.  The status word is
  * rewritten from scratch.  Host errors: RAG_ERR_ARG for null or misaligned
  * arrays and out-of-range host fields, RAG_ERR_CAPACITY if tile_cap exceeds
@@ -407,6 +418,11 @@ rag_status encoder_layer_workspace(int32_t total_tokens, int32_t max_len, int32_
  * projection, 5 LayerNorm 1, 6 FF1, 7 FF2, 8 LayerNorm 2.  With fused
  * attention (the default) stages 1 and 2 are empty and stage 3 holds the one
  * fused attention kernel.
+ * After a data error (a bit set in the plan's status word, by this call's
+ * own prelude or an earlier one) the attention stage writes nothing, while
+ * the token-wise stages (projections, LayerNorms) still run over the T rows
+ * the host declared: y then holds unspecified values and must be discarded.
+ * RAG_SYNC_CHECK=1 reports the condition as RAG_ERR_DATA.
  */
 rag_status encoder_layer(const rag_plan* plan, const void* x, void* y, int32_t d_model,
                          int32_t heads, int32_t head_dim, int32_t d_ff, float ln_eps, int32_t act,

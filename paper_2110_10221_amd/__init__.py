@@ -4,7 +4,7 @@ encoder layer for MI355X (gfx950).
 This module only marshals arguments: torch tensors provide device memory and
 the current HIP stream; every step of the computation runs in the library's HIP
 kernels.  There is no CPU path: importing fails loudly when the library has not
-been built (``python -m paper_2110_10221_amd._build`` or
+been built (``python paper_2110_10221_amd/_build.py`` or
 ``__graft_entry__.build()``).
 
 Function names match the C interface in include/ragged.h.
@@ -17,8 +17,7 @@ import os
 import torch
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-# RAG_LIBRARY selects an alternate build of the same library (e.g. a variant)
-LIB_PATH = os.environ.get("RAG_LIBRARY") or os.path.join(_HERE, "libragged.so")
+LIB_PATH = os.path.join(_HERE, "libragged.so")
 
 RAG_OK = 0
 RAG_F32, RAG_BF16 = 0, 1
@@ -38,7 +37,7 @@ VGEMM_DATA_BITS = {1: "negative size", 2: "size > RAG_VGEMM_MAX_DIM", 4: "tile_c
 
 if not os.path.exists(LIB_PATH):
     raise ImportError(f"{LIB_PATH} is missing: build the HIP library first "
-                      "(python -m paper_2110_10221_amd._build)")
+                      "(python paper_2110_10221_amd/_build.py)")
 
 _lib = ctypes.CDLL(LIB_PATH)
 
@@ -88,6 +87,7 @@ _c_attention_causal = _sig("ragged_attention_causal", list(_c_attention.argtypes
 _c_linear = _sig("packed_linear", [_p, _i32, _p, _p, _p, _i32, _i32, _p, _i32, _i32, _i32, _i32, _i32, _p])
 _c_layernorm = _sig("packed_layernorm", [_p, _i32, _p, _p, _f32, _p, _i32, _i32, _i32, _i32, _p])
 _c_vgemm_capacity = _sig("vgemm_plan_capacity", [_i32, _i32, _i32, ctypes.POINTER(_i64)])
+_c_vgemm_tile_count = _sig("vgemm_tile_count", [_i32, _p, ctypes.POINTER(_i64)])
 _c_vgemm_offsets = _sig("vgemm_offsets", [ctypes.POINTER(RagVgemmPlan), _p])
 _c_vgemm = _sig("ragged_vgemm", [ctypes.POINTER(RagVgemmPlan), _p, _i64, _p, _i64, _p, _i64, _i32, _p])
 _c_trmm = _sig("ragged_trmm", [_p, _i32, _p, _i32, _p, _i32, _i32, _i32, _i32, _p])
@@ -150,7 +150,11 @@ class Plan:
 
     def __init__(self, lengths: torch.Tensor, total_tokens: int, max_len: int, heads: int,
                  qkt_cap: int | None = None, av_cap: int | None = None):
-        if lengths.dtype != torch.int32 or not lengths.is_cuda or lengths.dim() != 1:
+        if lengths.dtype != torch.int32 or lengths.dim() != 1:
+            raise ValueError("lengths must be a 1-D int32 device tensor")
+        if not lengths.is_contiguous():
+            raise ValueError("lengths must be contiguous (the kernels read lengths[b] as dense memory)")
+        if not lengths.is_cuda:
             raise ValueError("lengths must be a 1-D int32 device tensor")
         dev = lengths.device
         B = lengths.numel()
@@ -282,6 +286,16 @@ def vgemm_plan_capacity(batch, max_m, max_n):
     return n.value
 
 
+def vgemm_tile_count(host_dims):
+    """Exact tile count of a batch from its (m, n, k) sizes held on the host."""
+    import numpy as np
+
+    d = np.ascontiguousarray(np.asarray(host_dims, dtype=np.int32).reshape(-1, 3))
+    n = _i64()
+    _check("vgemm_tile_count", _c_vgemm_tile_count(d.shape[0], d.ctypes.data_as(ctypes.c_void_p), ctypes.byref(n)))
+    return n.value
+
+
 class VgemmPlan:
     """Device arrays of a vgemm batch's prelude, allocated with torch.
 
@@ -298,8 +312,7 @@ class VgemmPlan:
         B = dims.shape[0]
         if tile_cap is None:
             if host_dims is not None:
-                tile_cap = sum(-(-max(int(m), 0) // RAG_VGEMM_TILE_M) * -(-max(int(n), 0) // RAG_VGEMM_TILE_N)
-                               for m, n, _ in host_dims)
+                tile_cap = vgemm_tile_count(host_dims)
             elif max_m is not None and max_n is not None:
                 tile_cap = vgemm_plan_capacity(B, max_m, max_n)
             else:

@@ -3,6 +3,7 @@
 #include <hip/hip_runtime.h>
 
 #include <atomic>
+#include <cmath>
 #include <cstdarg>
 #include <cstdio>
 #include <cstdlib>
@@ -186,6 +187,7 @@ rag_status qkt_impl(const rag_plan* plan, const void* q, int32_t ldq, const void
     const int64_t width = (int64_t)plan->heads * head_dim;
     if ((st = check_operand(q, ldq, width, dtype, 16, "q", fn)) || (st = check_operand(k, ldk, width, dtype, 16, "k", fn)))
         return st;
+    if (!std::isfinite(scale)) return fail(RAG_ERR_ARG, "%s: scale is not finite", fn);
     if (!scores || score_cap < 0) return fail(RAG_ERR_ARG, "%s: scores is NULL or score_cap < 0", fn);
     if (!aligned(scores, elem_size(dtype))) return fail(RAG_ERR_ARG, "%s: scores misaligned", fn);
     hipStream_t s = static_cast<hipStream_t>(stream);
@@ -232,6 +234,7 @@ rag_status attention_impl(const rag_plan* plan, const void* q, int32_t ldq, cons
     if ((st = check_operand(q, ldq, width, dtype, 16, "q", fn)) || (st = check_operand(k, ldk, width, dtype, 16, "k", fn)) ||
         (st = check_operand(vv, ldv, width, dtype, 16, "v", fn)) || (st = check_operand(out, ldo, width, dtype, 16, "out", fn)))
         return st;
+    if (!std::isfinite(scale)) return fail(RAG_ERR_ARG, "%s: scale is not finite", fn);
     if (!fused_fits(plan->max_len, ldk > ldv ? ldk : ldv))
         return fail(RAG_ERR_SHAPE, "%s: max_len %d rows of leading dimension %d exceed the kernel's 32-bit offsets", fn,
                     plan->max_len, ldk > ldv ? ldk : ldv);
@@ -513,6 +516,23 @@ rag_status vgemm_plan_capacity(int32_t batch, int32_t max_m, int32_t max_n, int6
         return fail(RAG_ERR_ARG, "%s: sizes out of range", fn);
     *tile_cap = (int64_t)batch * ((max_m + RAG_VGEMM_TILE_M - 1) / RAG_VGEMM_TILE_M) *
                 ((max_n + RAG_VGEMM_TILE_N - 1) / RAG_VGEMM_TILE_N);
+    return RAG_OK;
+}
+
+rag_status vgemm_tile_count(int32_t batch, const int32_t* dims, int64_t* tiles) {
+    const char* fn = "vgemm_tile_count";
+    if (!dims || !tiles) return fail(RAG_ERR_ARG, "%s: dims or tiles is NULL", fn);
+    if (batch < 1 || batch > RAG_VGEMM_MAX_BATCH)
+        return fail(RAG_ERR_ARG, "%s: batch %d outside [1, %d]", fn, batch, RAG_VGEMM_MAX_BATCH);
+    int64_t n = 0;
+    for (int32_t p = 0; p < batch; ++p) {
+        const int32_t m = dims[3 * p], nn = dims[3 * p + 1], k = dims[3 * p + 2];
+        if (m < 0 || nn < 0 || k < 0 || m > RAG_VGEMM_MAX_DIM || nn > RAG_VGEMM_MAX_DIM || k > RAG_VGEMM_MAX_DIM)
+            return fail(RAG_ERR_ARG, "%s: problem %d has sizes (%d, %d, %d) outside [0, %d]", fn, p, m, nn, k,
+                        RAG_VGEMM_MAX_DIM);
+        n += (int64_t)((m + RAG_VGEMM_TILE_M - 1) / RAG_VGEMM_TILE_M) * ((nn + RAG_VGEMM_TILE_N - 1) / RAG_VGEMM_TILE_N);
+    }
+    *tiles = n;
     return RAG_OK;
 }
 

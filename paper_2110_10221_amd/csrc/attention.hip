@@ -457,7 +457,10 @@ void k_attention_bf16(PlanArgs pa, const uint16_t* __restrict__ q, int ldq, cons
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave), lane = threadIdx.x % kWave;
     const int l32 = lane % 32, h2 = lane / 32;
     const int tr_e = (lane % 16) / 4, tr_q = lane % 4, tr_g = lane / 16;
-    const float zs = fabsf(scale) * 1.4426950408889634f;
+    // A zero scale would turn the masked keys' -inf into NaN (-inf * 0); any
+    // |scale| below 1e-30 already makes every exponential round to 1 (the
+    // uniform softmax of a zero scale), so the factor is kept at least that.
+    const float zs = fmaxf(fabsf(scale) * 1.4426950408889634f, 1e-30f);
     const uint32_t qsign = scale < 0.f ? 0x80008000u : 0u;
     // a stage holds keys 32c .. 32c + 31 at rows 0..31; 32c leaves the swizzle's
     // row bits 1-3 unchanged, so the offsets are those of chunk 0

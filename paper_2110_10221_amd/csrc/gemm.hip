@@ -541,6 +541,7 @@ __device__ __forceinline__ void gemm_tile_bf16(const uint16_t* __restrict__ x, i
 // QKV projection carries the prelude that way, in the slots its last round of
 // tiles leaves free.
 static_assert(sizeof(PlanSmem) <= tile_lds_bytes<64, false>(), "the plan's LDS fits the GEMM's");
+static_assert(Cfg<128>::kThreads == kFusedBatch, "the plan body runs one thread per sequence of a full batch");
 
 template <int ACT, bool HAS_BIAS, bool HAS_RES>
 __global__ __launch_bounds__(Cfg<128>::kThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
@@ -629,10 +630,7 @@ __global__ __launch_bounds__(256) void k_gemm_f32(const float* __restrict__ x, i
 // problem and share its operand panels in that XCD's L2, while every XCD still
 // gets a share of the large problems first.
 // ---------------------------------------------------------------------------
-#ifndef RAG_VGEMM_CHUNK
-#define RAG_VGEMM_CHUNK 32
-#endif
-constexpr int kVgemmChunk = RAG_VGEMM_CHUNK;
+constexpr int kVgemmChunk = 32;
 constexpr int kVgemmGridQuantum = 8 * kVgemmChunk;  // the grid is a multiple of this
 
 struct VgemmArgs {

@@ -113,10 +113,14 @@ def test_host_validation_rejects_bad_arguments():
     assert lib.ragged_qkt(plan, None, 128, q, 128, 64, 0.125, q, 10, 1, s) == ERR_ARG
     assert lib.ragged_qkt(plan, q, 128, q, 128, 64, 0.125, None, 10, 1, s) == ERR_ARG
     assert lib.ragged_qkt(plan, q, 128, q, 128, 64, 0.125, q, -1, 1, s) == ERR_ARG
+    assert lib.ragged_qkt(plan, q, 128, q, 128, 64, float("nan"), q, 10, 1, s) == ERR_ARG   # scale not finite
+    assert lib.ragged_qkt(plan, q, 128, q, 128, 64, float("inf"), q, 10, 1, s) == ERR_ARG
 
     lib.ragged_attention.argtypes = [P, P, ctypes.c_int32, P, ctypes.c_int32, P, ctypes.c_int32, ctypes.c_int32,
                                      ctypes.c_float, P, ctypes.c_int32, ctypes.c_int32, P]
     assert lib.ragged_attention(plan, q, 128, q, 128, q, 128, 64, 0.1, q, 128, 0, s) == ERR_DTYPE  # bf16 only
+    assert lib.ragged_attention(plan, q, 128, q, 128, q, 128, 64, float("nan"), q, 128, 1, s) == ERR_ARG
+    assert b"scale" in lib.ragged_last_error()
 
     # packed_linear(x, ldx, w, bias, res, ldr, act, y, ldy, T, K, N, dtype, stream)
     lib.packed_linear.argtypes = [P, ctypes.c_int32, P, P, P, ctypes.c_int32, ctypes.c_int32, P, ctypes.c_int32,
@@ -184,6 +188,36 @@ def test_vgemm_plan_struct_and_capacity():
     assert rag.vgemm_plan_capacity(2, 129, 256) == 2 * 2 * 1
     with pytest.raises(rag.RaggedError, match="RAG_ERR_ARG"):
         rag.vgemm_plan_capacity(0, 128, 128)
+
+
+@needs_lib
+def test_vgemm_tile_count_matches_the_oracle_prefix():
+    import numpy as np
+    import paper_2110_10221_amd as rag
+
+    for seed in range(4):
+        rng = np.random.default_rng(seed)
+        dims = rng.integers(0, 3000, size=(int(rng.integers(1, 80)), 3)).astype(np.int32)
+        dims[::7, 2] = 0  # k = 0 problems still own output tiles
+        assert rag.vgemm_tile_count(dims) == int(oracle.vgemm_offsets(dims).tile_off[-1])
+    assert rag.vgemm_tile_count([[128, 256, 64], [129, 257, 64], [0, 512, 64]]) == 1 + 4 + 0
+    with pytest.raises(rag.RaggedError, match="RAG_ERR_ARG"):
+        rag.vgemm_tile_count([[128, -1, 64]])
+    with pytest.raises(rag.RaggedError, match="RAG_ERR_ARG"):
+        rag.vgemm_tile_count([[rag.RAG_VGEMM_MAX_DIM + 1, 1, 1]])
+    with pytest.raises(rag.RaggedError, match="RAG_ERR_ARG"):
+        rag.vgemm_tile_count(np.zeros((0, 3), np.int32))
+
+
+@needs_lib
+def test_plan_rejects_non_contiguous_lengths():
+    import paper_2110_10221_amd as rag
+
+    L = torch.tensor([3, 5, 7, 9], dtype=torch.int32)
+    with pytest.raises(ValueError, match="contiguous"):
+        rag.Plan(L[::2], 10, 7, 2)
+    with pytest.raises(ValueError, match="contiguous"):
+        rag.Plan(torch.tensor([4], dtype=torch.int32).expand(8), 32, 4, 2)
 
 
 @needs_lib

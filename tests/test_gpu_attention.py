@@ -232,6 +232,33 @@ def test_fused_attention_negative_scale():
     _fused_close(got, L, H, q, k, v, -0.2)
 
 
+@pytest.mark.parametrize("scale", [0.0, -0.0])
+def test_fused_attention_zero_scale_is_uniform(scale):
+    # a zero scale makes every score 0 and the softmax uniform over the row's
+    # keys; lengths that leave the last 32-key chunk partial, masked keys included
+    rng = np.random.default_rng(12)
+    L = np.array([1, 5, 33, 70, 130], np.int32)
+    T, H = int(L.sum()), 2
+    q, k, v = (random_storage(rng, (T, H * 64), "bf16", 1.0) for _ in range(3))
+    got = _fused(L, H, q, k, v, scale)
+    assert np.all(np.isfinite(values(got, "bf16")))
+    _fused_close(got, L, H, q, k, v, scale)
+    # the oracle chain gives the mean of each sequence's V rows, elementwise
+    st = np.concatenate([[0], np.cumsum(L)])
+    vv = values(v, "bf16").reshape(T, H * 64)
+    mean = np.concatenate([np.repeat(vv[st[b]:st[b + 1]].mean(0, keepdims=True), L[b], 0) for b in range(len(L))])
+    g = values(got, "bf16").reshape(T, H * 64)
+    assert np.abs(g - mean).max() <= 1e-3 + 2e-2 * np.abs(vv).max()
+
+
+def test_unfused_attention_zero_scale_matches_oracle():
+    rng = np.random.default_rng(13)
+    L, H = np.array([3, 64, 100], np.int32), 2
+    T = int(L.sum())
+    q, k, v = (random_storage(rng, (T, H * 64), "bf16", 1.0) for _ in range(3))
+    _check_ops(L, H, q, k, v, "bf16", 0.0)
+
+
 def test_score_buffer_too_small_is_reported_not_written():
     import paper_2110_10221_amd as rag
 
