@@ -430,6 +430,25 @@ rag_status encoder_layer(const rag_plan* plan, const void* x, void* y, int32_t d
                          size_t workspace_bytes, int32_t dtype, void* stream,
                          void* const* events);
 
+/*
+ * encoder_layer for callers that cannot allocate device memory (code under HIP
+ * graph capture, tight serving loops, harnesses that forbid allocation): the
+ * same layer, arguments, results and errors as encoder_layer with events ==
+ * NULL, but its workspace is a fixed device array of RAG_NOALLOC_SCRATCH_BYTES
+ * inside the library (each GPU the library runs on holds its own copy until the
+ * process ends).  The call allocates nothing.  RAG_ERR_WORKSPACE if the layer
+ * would need more than that (encoder_layer_workspace gives the size), checked
+ * on the host before anything launches.  Every call on one GPU shares that
+ * GPU's array, so calls that overlap in time on one GPU (different streams or
+ * host threads without ordering between them) race and must not be issued;
+ * calls ordered on one stream are fine.  The array needs no clearing: the layer
+ * writes every intermediate element before reading it.
+ */
+#define RAG_NOALLOC_SCRATCH_BYTES (64u << 20)
+rag_status encoder_layer_noalloc(const rag_plan* plan, const void* x, void* y, int32_t d_model,
+                                 int32_t heads, int32_t head_dim, int32_t d_ff, float ln_eps, int32_t act,
+                                 int32_t flags, const rag_layer_weights* w, int32_t dtype, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

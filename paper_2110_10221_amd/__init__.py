@@ -28,6 +28,7 @@ RAG_LAYER_UNFUSED_ATTENTION = 1
 RAG_LAYER_CAUSAL = 2
 RAG_LAYER_BUILD_PLAN = 4
 RAG_LAYER_EVENTS = 10
+RAG_NOALLOC_SCRATCH_BYTES = 64 << 20
 DATA_BITS = {1: "negative length", 2: "length > max_len", 4: "sum of lengths != total_tokens",
              8: "qkt_cap exceeded", 16: "av_cap exceeded", 32: "score buffer too small"}
 RAG_VGEMM_TILE_M, RAG_VGEMM_TILE_N = 128, 256
@@ -94,6 +95,8 @@ _c_trmm = _sig("ragged_trmm", [_p, _i32, _p, _i32, _p, _i32, _i32, _i32, _i32, _
 _c_ws = _sig("encoder_layer_workspace", [_i32, _i32, _i32, _i32, _i32, _i32, _i32, ctypes.POINTER(ctypes.c_size_t)])
 _c_layer = _sig("encoder_layer", [ctypes.POINTER(RagPlan), _p, _p, _i32, _i32, _i32, _i32, _f32, _i32, _i32,
                                   ctypes.POINTER(RagLayerWeights), _p, ctypes.c_size_t, _i32, _p, _p])
+_c_layer_noalloc = _sig("encoder_layer_noalloc", [ctypes.POINTER(RagPlan), _p, _p, _i32, _i32, _i32, _i32, _f32,
+                                                  _i32, _i32, ctypes.POINTER(RagLayerWeights), _i32, _p])
 
 
 class RaggedError(RuntimeError):
@@ -278,6 +281,17 @@ def encoder_layer(plan: Plan, x, y, weights, d_ff, workspace, heads=None, head_d
                                      ctypes.byref(w), _ptr(workspace), workspace.numel() * workspace.element_size(),
                                      _dtype_code(x), _stream(stream),
                                      None if events is None else ctypes.cast(events, ctypes.c_void_p)))
+
+
+def encoder_layer_noalloc(plan: Plan, x, y, weights, d_ff, heads=None, head_dim=RAG_HEAD_DIM, ln_eps=1e-5,
+                          act=RAG_ACT_GELU_ERF, flags=0, stream=None):
+    """encoder_layer with the library's fixed device scratch array as its workspace
+    (RAG_NOALLOC_SCRATCH_BYTES): no workspace argument, nothing allocated."""
+    T, d = x.shape
+    heads = plan.heads if heads is None else heads
+    w = weights if isinstance(weights, RagLayerWeights) else layer_weights(weights)
+    _check("encoder_layer_noalloc", _c_layer_noalloc(plan.ref(), _ptr(x), _ptr(y), d, heads, head_dim, d_ff, ln_eps,
+                                                     act, flags, ctypes.byref(w), _dtype_code(x), _stream(stream)))
 
 
 def vgemm_plan_capacity(batch, max_m, max_n):

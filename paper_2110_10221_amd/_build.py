@@ -17,7 +17,7 @@ INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(HERE, "libragged.so")
 OBJ_DIR = os.path.join(ROOT, "_build", "ragged")
 
-SOURCES = ["api.cpp", "offsets.hip", "attention.hip", "gemm.hip", "layernorm.hip"]
+SOURCES = ["api.cpp", "offsets.hip", "attention.hip", "gemm.hip", "layernorm.hip", "noalloc.hip"]
 ARCH = "gfx950"
 
 COMMON = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}", "-I", INCLUDE, "-I", CSRC,

@@ -6,6 +6,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "../../include/ragged.h"
+
 namespace rag {
 
 struct PlanView {
@@ -25,6 +27,9 @@ struct PlanView {
 
 // Number of compute units of the current device (cached per device).
 int device_cu_count();
+
+// Record a formatted message as the thread's last error and return `status`.
+rag_status report(rag_status status, const char* fmt, ...);
 
 hipError_t launch_offsets(const PlanView& p, hipStream_t s);
 
