@@ -62,6 +62,10 @@ rag_status finish(hipError_t launch_err, hipStream_t s, const int32_t* status, c
 // byte offsets from the sequence's first row.
 bool fused_fits(int64_t max_len, int64_t ld) { return max_len * ld * 2 <= INT32_MAX; }
 
+// The bf16 attention operators address one item's scores (64 query rows of
+// heads * max_len values) with 32-bit byte offsets.
+bool op_item_fits(int64_t heads, int64_t max_len) { return 64 * heads * max_len * 2 + 64 <= INT32_MAX; }
+
 rag_status view_plan(const rag_plan* p, rag::PlanView& v, const char* fn) {
     if (!p) return fail(RAG_ERR_ARG, "%s: plan is NULL", fn);
     if (p->batch < 1 || p->batch > RAG_MAX_BATCH)
@@ -197,6 +201,8 @@ rag_status qkt_impl(const rag_plan* plan, const void* q, int32_t ldq, const void
         return st;
     if (!std::isfinite(scale)) return fail(RAG_ERR_ARG, "%s: scale is not finite", fn);
     if (!scores || score_cap < 0) return fail(RAG_ERR_ARG, "%s: scores is NULL or score_cap < 0", fn);
+    if (dtype == RAG_BF16 && !op_item_fits(plan->heads, plan->max_len))
+        return fail(RAG_ERR_SHAPE, "%s: 64 * heads * max_len * 2 bytes exceeds 32-bit item offsets", fn);
     if (!aligned(scores, elem_size(dtype))) return fail(RAG_ERR_ARG, "%s: scores misaligned", fn);
     hipStream_t s = static_cast<hipStream_t>(stream);
     return finish(rag::launch_qkt(v, dtype, q, ldq, k, ldk, scale, scores, score_cap, causal, s), s, plan->status, fn);
@@ -226,6 +232,8 @@ rag_status attn_v_impl(const rag_plan* plan, const void* probs, int64_t score_ca
         return st;
     if (!probs || score_cap < 0) return fail(RAG_ERR_ARG, "%s: probs is NULL or score_cap < 0", fn);
     if (!aligned(probs, elem_size(dtype))) return fail(RAG_ERR_ARG, "%s: probs misaligned", fn);
+    if (dtype == RAG_BF16 && !op_item_fits(plan->heads, plan->max_len))
+        return fail(RAG_ERR_SHAPE, "%s: 64 * heads * max_len * 2 bytes exceeds 32-bit item offsets", fn);
     hipStream_t s = static_cast<hipStream_t>(stream);
     return finish(rag::launch_attn_v(v, dtype, probs, score_cap, vv, ldv, out, ldo, causal, s), s, plan->status, fn);
 }
@@ -427,6 +435,8 @@ rag_status encoder_layer(const rag_plan* plan, const void* x, void* y, int32_t d
     if (flags & ~(RAG_LAYER_UNFUSED_ATTENTION | RAG_LAYER_CAUSAL | RAG_LAYER_BUILD_PLAN))
         return fail(RAG_ERR_ARG, "%s: unknown flags 0x%x", fn, flags);
     const int T = plan->total_tokens, d = d_model;
+    if (dtype == RAG_BF16 && unfused_attention(dtype, flags, plan->max_len, d) && !op_item_fits(heads, plan->max_len))
+        return fail(RAG_ERR_SHAPE, "%s: 64 * heads * max_len * 2 bytes exceeds 32-bit item offsets", fn);
     const LayerBuffers lb = layer_buffers(T, plan->max_len, d, heads, d_ff, dtype, flags);
     if (!workspace || workspace_bytes < lb.total)
         return fail(RAG_ERR_WORKSPACE, "%s: workspace of %zu bytes given, %zu needed", fn, workspace_bytes, lb.total);

@@ -32,13 +32,15 @@ struct PlanArgs {
     const int32_t* tok_seq;
     const int32_t* qkt_items;
     const int32_t* av_items;
+    const int32_t* order;
+    const int32_t* av_item_off;
     int32_t* status;
     int batch, heads;
 };
 
 PlanArgs plan_args(const PlanView& p) {
-    return PlanArgs{p.lengths, p.tok_off, p.att_off, p.tok_seq, p.qkt_items, p.av_items, p.status,
-                    p.batch, p.heads};
+    return PlanArgs{p.lengths, p.tok_off, p.att_off, p.tok_seq, p.qkt_items, p.av_items, p.order, p.av_item_off,
+                    p.status, p.batch, p.heads};
 }
 
 // True if the plan is valid and the score buffer large enough; otherwise one
@@ -54,61 +56,201 @@ __device__ __forceinline__ bool plan_ok(const PlanArgs& pa, int64_t score_cap) {
 
 __device__ __forceinline__ u32x4 ld16(const uint16_t* p) { return *reinterpret_cast<const u32x4*>(p); }
 
+// The status word is written in these kernels (atomicOr), so the compiler cannot
+// keep plan reads in scalar registers by itself; values that are uniform over the
+// workgroup are made so explicitly (a buffer descriptor built from a per-lane value
+// becomes a loop over lanes).
+__device__ __forceinline__ int uni(int v) { return __builtin_amdgcn_readfirstlane(v); }
+__device__ __forceinline__ int64_t uni64(int64_t v) {
+    const uint32_t lo = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(v));
+    const uint32_t hi = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(static_cast<uint64_t>(v) >> 32));
+    return static_cast<int64_t>((static_cast<uint64_t>(hi) << 32) | lo);
+}
+
 // ---------------------------------------------------------------------------
 // QK^T
 // ---------------------------------------------------------------------------
 
 constexpr int kStage = kTile + 8;  // padded LDS row (elements)
 
-// One item per (sequence, head, 64-query block) from the Attn.V work list: the
-// block's Q fragments are loaded once and the item walks every key tile of the
-// row, so the 128-byte pieces of each score row are written back to back by one
-// workgroup (the L2 can merge them into whole lines before they reach HBM).
+// The bf16 operators take one work item per (sequence, 64-query block, group of
+// G consecutive heads), G a divisor of H chosen at launch so that the batch
+// makes enough items to fill the GPU.  In the X[b][i][h][j] layout the item's
+// scores are G * L_b contiguous values per query row (all of them, one region,
+// when G = H), so a workgroup reads or writes whole cache lines, and the item
+// reads each of its heads' K (or V) panels of the sequence once.  Items follow
+// the plan's Attn.V list (sequences longest first, then head groups, then query
+// blocks); a workgroup finds its item's sequence by a wave-wide search of the
+// per-sequence item prefix, and consecutive items (the query blocks of one head
+// group) go to one XCD in runs, so they share its K / V panels in that L2.
+constexpr int kOpRun = 8;  // consecutive items per XCD
+
+// Largest k with off[k] / G <= g: the sorted sequence holding item g (off holds
+// H entries per 64-query block of each sequence, so off[k] / G counts the items
+// of G heads each, G a divisor of H).
+__device__ __forceinline__ int item_sequence(const int32_t* off, int B, int G, int g) {
+    const int lane = threadIdx.x % kWave;
+    int lo = 0, span = B;
+    while (span > 1) {
+        const int st = (span + kWave - 1) / kWave;
+        const bool le = lane * st < span && off[lo + lane * st] / G <= g;
+        const uint64_t m = __ballot(le);  // lane 0 always holds (off[lo] / G <= g)
+        const int last = 63 - __builtin_clzll(m);
+        lo += last * st;
+        span = min(st, span - last * st);
+    }
+    return lo;
+}
+
+__device__ __forceinline__ int op_item(int bid, int grid) {  // grid: a multiple of 8 * kOpRun
+    const int xcd = bid % 8, j = bid / 8;
+    return ((j / kOpRun) * 8 + xcd) * kOpRun + j % kOpRun;
+}
+
+// Elements s .. s + 7 of the 16 elements a:b (s in [0, 8)), i.e. bytes [2s, 2s + 16).
+__device__ __forceinline__ u32x4 window16(const u32x4& a, const u32x4& b, int s) {
+    const int q = s >> 1;
+    uint32_t d[5];
+#pragma unroll
+    for (int k = 0; k < 5; ++k) {
+        const uint32_t w0 = k < 4 ? a[k] : b[k - 4];
+        const uint32_t w1 = k + 1 < 4 ? a[k + 1] : b[k - 3];
+        const uint32_t w2 = k + 2 < 4 ? a[k + 2] : b[k - 2];
+        const uint32_t w3 = k + 3 < 4 ? a[k + 3] : b[k - 1];
+        d[k] = q == 0 ? w0 : q == 1 ? w1 : q == 2 ? w2 : w3;
+    }
+    u32x4 o;
+    if (s & 1) {
+#pragma unroll
+        for (int k = 0; k < 4; ++k) o[k] = __builtin_amdgcn_alignbyte(d[k + 1], d[k], 2);
+    } else {
+#pragma unroll
+        for (int k = 0; k < 4; ++k) o[k] = d[k];
+    }
+    return o;
+}
+
+// bf16 QK^T.  Per head of the item and piece of kPiece keys, wave w computes the
+// piece's key tile w for all 64 query rows of the block (v_mfma_f32_16x16x32_bf16,
+// K fragments straight from memory, the next piece's tile loaded while this one
+// is computed), scaled and rounded into the workgroup's LDS rows; then all
+// threads write the piece's row pieces as aligned 16-byte chunks (a row starts at
+// any element, so a chunk is cut from two LDS chunks by a funnel shift), and
+// 2-byte stores for the partial chunks at both ends of each row piece.
+constexpr int kPiece = 4 * kTile;         // keys per written row piece: one tile per wave
+constexpr int kPieceRow = kPiece + 8;     // LDS row (elements): room for the shifted read, 4-bank row skew
 __global__ __launch_bounds__(256) void k_qkt_bf16(PlanArgs pa, const uint16_t* __restrict__ q, int ldq,
                                                    const uint16_t* __restrict__ k, int ldk, float scale,
-                                                   uint16_t* __restrict__ S, int64_t score_cap, int causal) {
+                                                   uint16_t* __restrict__ S, int64_t score_cap, int causal, int G) {
     if (!plan_ok(pa, score_cap)) return;
-    __shared__ uint16_t tile[kTile][kStage];
-    const int n_items = pa.status[2];
+    __shared__ __attribute__((aligned(16))) uint16_t st[kTile][kPieceRow];
     const int H = pa.heads;
+    const int n_items = pa.status[2] / G, ng = H / G;
     const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
     const int l16 = lane % 16, q4 = lane / 16;
-    for (int it = blockIdx.x; it < n_items; it += gridDim.x) {
-        const int b = pa.av_items[3 * it], h = pa.av_items[3 * it + 1], ti = pa.av_items[3 * it + 2];
-        const int L = pa.lengths[b];
-        const int t0 = pa.tok_off[b];
-        const int64_t base = pa.att_off[b];
-        // this wave: query rows ti*64 + wave*16 .. +15
-        const int qi = min(ti * kTile + wave * 16 + l16, L - 1);
-        const uint16_t* qrow = q + (int64_t)(t0 + qi) * ldq + h * kHeadDim + 8 * q4;
-        const bf16x8 qa0 = as_bf16x8(ld16(qrow)), qa1 = as_bf16x8(ld16(qrow + 32));
-        const int rows = min(kTile, L - ti * kTile);
-        const int n_tj = causal ? ti + 1 : (L + kTile - 1) / kTile;  // masked: key tiles up to the diagonal
-        for (int tj = 0; tj < n_tj; ++tj) {
-            floatx4 acc[4];
+    for (int base_it = 0; base_it < n_items; base_it += gridDim.x) {
+        const int g = base_it + op_item(blockIdx.x, gridDim.x);
+        if (g >= n_items) break;
+        const int kk = uni(item_sequence(pa.av_item_off, pa.batch, G, g));
+        const int b = uni(pa.order[kk]);
+        const int local = g - uni(pa.av_item_off[kk]) / G;
+        const int nb = (uni(pa.lengths[b]) + kTile - 1) / kTile;  // query blocks of the sequence
+        const int hg = local / nb, ti = local - hg * nb, h0 = hg * G;  // heads h0 .. h0 + G - 1
+        const int L = uni(pa.lengths[b]);
+        const int t0 = uni(pa.tok_off[b]);
+        const int64_t base = uni64(pa.att_off[b]);
+        const int i0 = ti * kTile;                // the block's first query row
+        const int rows = min(kTile, L - i0);
+        // keys the block needs: all, or (masked) up to its last row
+        const int kend = causal ? min(L, i0 + rows) : L;
+        const int npc = (kend + kPiece - 1) / kPiece;  // pieces per head
+        const int F = G * npc;
+        // this wave's key tile of piece f: head h0 + f / npc, keys (f % npc) * kPiece + 64 wave ..
+        bf16x8 kc[4][2], kn[4][2], qf[4][2];
+        auto load_k = [&](int f, bf16x8 (&kb)[4][2]) {
+            const int h = h0 + f / npc, k0 = (f % npc) * kPiece + wave * kTile;
 #pragma unroll
             for (int jb = 0; jb < 4; ++jb) {
-                const int kj = min(tj * kTile + jb * 16 + l16, L - 1);
+                const int kj = min(k0 + jb * 16 + l16, L - 1);
                 const uint16_t* krow = k + (int64_t)(t0 + kj) * ldk + h * kHeadDim + 8 * q4;
-                const bf16x8 kb0 = as_bf16x8(ld16(krow)), kb1 = as_bf16x8(ld16(krow + 32));
-                acc[jb] = floatx4{0.f, 0.f, 0.f, 0.f};
-                acc[jb] = mfma16x16x32(kb0, qa0, acc[jb]);  // C[j][i] = sum_c K[j][c] Q[i][c]
-                acc[jb] = mfma16x16x32(kb1, qa1, acc[jb]);
+                kb[jb][0] = as_bf16x8(ld16(krow));
+                kb[jb][1] = as_bf16x8(ld16(krow + 32));
             }
-            __syncthreads();  // the previous tile's stores have read the staging tile
+        };
+        load_k(0, kc);
+        for (int f = 0; f < F; ++f) {
+            const int h = h0 + f / npc, p0 = (f % npc) * kPiece;
+            if (f % npc == 0) {  // a new head: its Q fragments, rows rg*16 + l16
 #pragma unroll
-            for (int jb = 0; jb < 4; ++jb)
+                for (int rg = 0; rg < 4; ++rg) {
+                    const int qi = min(i0 + rg * 16 + l16, L - 1);
+                    const uint16_t* qrow = q + (int64_t)(t0 + qi) * ldq + h * kHeadDim + 8 * q4;
+                    qf[rg][0] = as_bf16x8(ld16(qrow));
+                    qf[rg][1] = as_bf16x8(ld16(qrow + 32));
+                }
+            }
+            if (f + 1 < F) load_k(f + 1, kn);
+            const int pn = min(kPiece, kend - p0);
+            const bool mine = wave * kTile < pn;  // this wave's tile holds keys of the piece
+            floatx4 acc[4][4];
+            if (mine) {
 #pragma unroll
-                for (int r = 0; r < 4; ++r)
-                    tile[wave * 16 + l16][jb * 16 + 4 * q4 + r] = f32_to_bf16(acc[jb][r] * scale);
+                for (int jb = 0; jb < 4; ++jb)
+#pragma unroll
+                    for (int rg = 0; rg < 4; ++rg) {
+                        acc[jb][rg] = floatx4{0.f, 0.f, 0.f, 0.f};
+                        acc[jb][rg] = mfma16x16x32(kc[jb][0], qf[rg][0], acc[jb][rg]);  // C[j][i] = K[j] . Q[i]
+                        acc[jb][rg] = mfma16x16x32(kc[jb][1], qf[rg][1], acc[jb][rg]);
+                    }
+            }
+            __syncthreads();  // the previous piece's LDS rows are written out
+            if (mine) {
+#pragma unroll
+                for (int jb = 0; jb < 4; ++jb)
+#pragma unroll
+                    for (int rg = 0; rg < 4; ++rg)
+                        *reinterpret_cast<u32x2*>(&st[rg * 16 + l16][wave * kTile + jb * 16 + 4 * q4]) =
+                            u32x2{pack_bf16x2(acc[jb][rg][0] * scale, acc[jb][rg][1] * scale),
+                                  pack_bf16x2(acc[jb][rg][2] * scale, acc[jb][rg][3] * scale)};
+            }
             __syncthreads();
-            const int cols = min(kTile, L - tj * kTile);
-            // masked: only keys j <= i are written (the diagonal tile's upper part is left alone)
-            const int jmax = causal ? ti * kTile - tj * kTile : kTile;
-            for (int rr = wave; rr < rows; rr += 4)
-                if (lane < cols && lane <= jmax + rr)
-                    S[base + ((int64_t)(ti * kTile + rr) * H + h) * L + tj * kTile + lane] = tile[rr][lane];
+            // Row r holds keys p0 .. p0 + n_r - 1 at elements G_r .. of S.  Pass 1: its
+            // whole 16-byte chunks (row r owns task slots r*M .. r*M + M - 1, M >= the
+            // chunks of any row); pass 2: the partial chunks at both ends of every row.
+            const int M = (pn >> 3) + 1;
+            const int64_t grow = base + ((int64_t)i0 * H + h) * L + p0;  // row 0's first element
+            for (int t = threadIdx.x; t < rows * M; t += 256) {
+                const int r = t / M, cl = t - r * M;
+                const int n = causal ? min(pn, i0 + r + 1 - p0) : pn;
+                const int64_t G0 = grow + (int64_t)r * H * L;
+                const int64_t c = ((G0 + 7) >> 3) + cl;
+                if (n > 0 && c < ((G0 + n) >> 3)) {
+                    const int j0 = (int)(8 * c - G0);  // first key (local) of the chunk
+                    const int a0 = j0 & ~7;
+                    const u32x4 lo4 = *reinterpret_cast<const u32x4*>(&st[r][a0]);
+                    const u32x4 hi4 = *reinterpret_cast<const u32x4*>(&st[r][a0 + 8]);
+                    *reinterpret_cast<u32x4*>(S + 8 * c) = window16(lo4, hi4, j0 & 7);
+                }
+            }
+            if (threadIdx.x < 2 * rows) {
+                const int r = threadIdx.x >> 1, tail = threadIdx.x & 1;
+                const int n = causal ? min(pn, i0 + r + 1 - p0) : pn;
+                const int64_t G0 = grow + (int64_t)r * H * L;
+                const int64_t fa = (G0 + 7) >> 3, fb = (G0 + n) >> 3;
+                const int head = (int)max<int64_t>(min<int64_t>(8 * fa - G0, n), 0);
+                const int e0 = tail ? (int)max<int64_t>(8 * fb - G0, head) : 0;
+                const int e1 = tail ? max(n, 0) : head;
+                for (int e = e0; e < e1; ++e) S[G0 + e] = st[r][e];
+            }
+            if (f + 1 < F) {
+#pragma unroll
+                for (int jb = 0; jb < 4; ++jb) {
+                    kc[jb][0] = kn[jb][0];
+                    kc[jb][1] = kn[jb][1];
+                }
+            }
         }
+        __syncthreads();  // the last piece's rows are written out before the next item stages
     }
 }
 
@@ -261,69 +403,141 @@ __global__ __launch_bounds__(256) void k_softmax(PlanArgs pa, const typename Ele
 // Attn.V
 // ---------------------------------------------------------------------------
 
+// bf16 Attn.V over the same items as QK^T (one sequence's 64-query block, all
+// heads): the probabilities of the item are one contiguous region; each lane
+// reads its 8 keys of a probability row as two aligned 16-byte chunks
+// (range-checked buffer loads) and a funnel shift.  V tiles are staged
+// transposed in LDS for all four waves.
 __global__ __launch_bounds__(256) void k_attn_v_bf16(PlanArgs pa, const uint16_t* __restrict__ P,
                                                       int64_t score_cap, const uint16_t* __restrict__ v,
-                                                      int ldv, uint16_t* __restrict__ O, int ldo, int causal) {
+                                                      int ldv, uint16_t* __restrict__ O, int ldo, int causal,
+                                                      int G) {
     if (!plan_ok(pa, score_cap)) return;
-    __shared__ __attribute__((aligned(16))) uint16_t Ps[kTile][kStage];  // [i][j]
     __shared__ __attribute__((aligned(16))) uint16_t Vt[kTile][kStage];  // [c][j]
-    const int n_items = pa.status[2];
     const int H = pa.heads;
+    const int n_items = pa.status[2] / G, ng = H / G;
     const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
     const int l16 = lane % 16, q4 = lane / 16;
-    for (int it = blockIdx.x; it < n_items; it += gridDim.x) {
-        const int b = pa.av_items[3 * it], h = pa.av_items[3 * it + 1], ti = pa.av_items[3 * it + 2];
-        const int L = pa.lengths[b];
-        const int t0 = pa.tok_off[b];
-        const int64_t base = pa.att_off[b];
+    for (int base_it = 0; base_it < n_items; base_it += gridDim.x) {
+        const int g = base_it + op_item(blockIdx.x, gridDim.x);
+        if (g >= n_items) break;  // uniform over the workgroup
+        const int kk = uni(item_sequence(pa.av_item_off, pa.batch, G, g));
+        const int b = uni(pa.order[kk]);
+        const int local = g - uni(pa.av_item_off[kk]) / G;
+        const int nb = (uni(pa.lengths[b]) + kTile - 1) / kTile;  // query blocks of the sequence
+        const int hg = local / nb, ti = local - hg * nb, h0 = hg * G;  // heads h0 .. h0 + G - 1
+        const int L = uni(pa.lengths[b]);
+        const int t0 = uni(pa.tok_off[b]);
+        const int64_t base = uni64(pa.att_off[b]);
         const int rows = min(kTile, L - ti * kTile);
-        floatx4 acc[4];
-#pragma unroll
-        for (int cb = 0; cb < 4; ++cb) acc[cb] = floatx4{0.f, 0.f, 0.f, 0.f};
+        const int i = ti * kTile + wave * 16 + l16;  // this lane's query row (valid if < ti*64 + rows)
+        const bool row_ok = wave * 16 + l16 < rows;
+        // the item reads rows ti*64 .. ti*64 + rows - 1 of heads h0 .. h0 + G - 1: from element e_lo on
+        const int64_t e_lo = base + (int64_t)ti * kTile * H * L;
+        const int64_t e_al = e_lo & ~(int64_t)7;
+        // Range: through the item's last element (a chunk read past it is masked), in
+        // whole dwords (the range check drops a dword that is only partly inside; a
+        // dword never straddles a page), and never past the caller's score_cap.
+        const int64_t e_end = min(score_cap, base + (int64_t)(ti * kTile + rows) * H * L);
+        const int64_t nbytes = min<int64_t>(((e_end - e_al) * 2 + 3) & ~(int64_t)3, (int64_t)0x7ffffffc);
+        const __amdgpu_buffer_rsrc_t rp =
+            __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(P + e_al), 0, (uint32_t)nbytes, 0x00020000);
         const int jend = causal ? min(L, (ti + 1) * kTile) : L;  // masked: keys up to the diagonal tile
-        for (int j0 = 0; j0 < jend; j0 += kTile) {
-            const int cols = min(kTile, L - j0);
-            __syncthreads();
-            // probabilities: rows i of the tile, keys j0..j0+63 (zero outside, and above the diagonal when masked)
-#pragma unroll 4
-            for (int r = 0; r < 16; ++r) {
-                const int i = threadIdx.x / kWave + 4 * r, j = lane;
-                uint16_t val = 0;
-                if (i < rows && j < cols && (!causal || j0 + j <= ti * kTile + i))
-                    val = P[base + ((int64_t)(ti * kTile + i) * H + h) * L + j0 + j];
-                Ps[i][j] = val;
+        const int kmax = causal ? min(L - 1, i) : L - 1;          // last key this row uses
+        // Tiles (head h0 + f / nt, keys 64 (f % nt) ..) in one stream: the V rows and
+        // probability chunks of tile f + 1 are loaded while tile f is computed.
+        const int nt = (jend + kTile - 1) / kTile;
+        const int F = G * nt;
+        u32x4 vr[2], vn[2], pr[2][2], pn[2][2];
+        auto load_v = [&](int f, u32x4 (&vv)[2]) {
+            const int h = h0 + f / nt, j0 = (f % nt) * kTile, cols = min(kTile, L - j0);
+#pragma unroll
+            for (int r = 0; r < 2; ++r) {
+                const int id = threadIdx.x + 256 * r;
+                const int jj = id >> 3, cc = (id & 7) * 8;
+                vv[r] = jj < cols ? ld16(v + (int64_t)(t0 + j0 + jj) * ldv + h * kHeadDim + cc) : u32x4{0u, 0u, 0u, 0u};
             }
+        };
+        // keys j0 + 32 ks + 8 q4 .. + 7 of this lane's row of head h: two aligned chunks
+        auto load_p = [&](int f, u32x4 (&pp)[2][2]) {
+            const int h = h0 + f / nt, j0 = (f % nt) * kTile;
+            const int64_t row_e = ((int64_t)(wave * 16 + l16) * H + h) * L;  // row start, relative to e_lo
+#pragma unroll
+            for (int ks = 0; ks < 2; ++ks) {
+                const int jk = j0 + 32 * ks + 8 * q4;
+                if (row_ok && jk <= kmax) {
+                    const int a0 = (int)(((e_lo - e_al) + row_e + jk) & ~(int64_t)7);
+                    pp[ks][0] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rp, a0 * 2, 0, 0));
+                    pp[ks][1] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rp, a0 * 2 + 16, 0, 0));
+                } else {
+                    pp[ks][0] = pp[ks][1] = u32x4{0u, 0u, 0u, 0u};
+                }
+            }
+        };
+        // the element shift of every row piece: row starts differ by multiples of L only
+        const int64_t row_e0 = (int64_t)(wave * 16 + l16) * H * L;
+        load_v(0, vr);
+        load_p(0, pr);
+        floatx4 acc[4];
+        for (int f = 0; f < F; ++f) {
+            const int h = h0 + f / nt, j0 = (f % nt) * kTile;
+            if (f % nt == 0) {
+#pragma unroll
+                for (int cb = 0; cb < 4; ++cb) acc[cb] = floatx4{0.f, 0.f, 0.f, 0.f};
+            }
+            __syncthreads();  // the previous tile's V reads are done
             // values: 64 keys x 64 channels, stored transposed [c][j]
 #pragma unroll
             for (int r = 0; r < 2; ++r) {
                 const int id = threadIdx.x + 256 * r;
                 const int jj = id >> 3, cc = (id & 7) * 8;
-                u32x4 vv = {0u, 0u, 0u, 0u};
-                if (jj < cols) vv = ld16(v + (int64_t)(t0 + j0 + jj) * ldv + h * kHeadDim + cc);
 #pragma unroll
                 for (int e = 0; e < 4; ++e) {
-                    Vt[cc + 2 * e][jj] = static_cast<uint16_t>(vv[e] & 0xffffu);
-                    Vt[cc + 2 * e + 1][jj] = static_cast<uint16_t>(vv[e] >> 16);
+                    Vt[cc + 2 * e][jj] = static_cast<uint16_t>(vr[r][e] & 0xffffu);
+                    Vt[cc + 2 * e + 1][jj] = static_cast<uint16_t>(vr[r][e] >> 16);
                 }
             }
             __syncthreads();
+            if (f + 1 < F) {
+                load_v(f + 1, vn);
+                load_p(f + 1, pn);
+            }
+            const int sh = (int)((e_lo - e_al + row_e0 + (int64_t)h * L + j0) & 7);
 #pragma unroll
             for (int ks = 0; ks < 2; ++ks) {
-                const bf16x8 pb = as_bf16x8(*reinterpret_cast<const u32x4*>(&Ps[wave * 16 + l16][32 * ks + 8 * q4]));
+                const int jk = j0 + 32 * ks + 8 * q4;
+                u32x4 pw = window16(pr[ks][0], pr[ks][1], sh);
+                // keys past the row's last used key count as zero
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const int j = jk + 2 * e;
+                    const uint32_t keep = (j <= kmax ? 0x0000ffffu : 0u) | (j + 1 <= kmax ? 0xffff0000u : 0u);
+                    pw[e] &= keep;
+                }
+                const bf16x8 pb = as_bf16x8(pw);
 #pragma unroll
                 for (int cb = 0; cb < 4; ++cb) {
                     const bf16x8 va = as_bf16x8(*reinterpret_cast<const u32x4*>(&Vt[cb * 16 + l16][32 * ks + 8 * q4]));
                     acc[cb] = mfma16x16x32(va, pb, acc[cb]);  // C[c][i] = sum_j V[j][c] P[i][j]
                 }
             }
-        }
-        const int i = wave * 16 + l16;
-        if (i < rows) {
-            uint16_t* orow = O + (int64_t)(t0 + ti * kTile + i) * ldo + h * kHeadDim;
+            if (f % nt == nt - 1 && row_ok) {
+                // C[c][i]: the lane holds channels cb*16 + 4 q4 .. + 3 of query row i
+                uint16_t* orow = O + (int64_t)(t0 + i) * ldo + h * kHeadDim;
 #pragma unroll
-            for (int cb = 0; cb < 4; ++cb) {
-                u32x2 w2 = {pack_bf16x2(acc[cb][0], acc[cb][1]), pack_bf16x2(acc[cb][2], acc[cb][3])};
-                *reinterpret_cast<u32x2*>(orow + cb * 16 + 4 * q4) = w2;
+                for (int cb = 0; cb < 4; ++cb) {
+                    u32x2 w2 = {pack_bf16x2(acc[cb][0], acc[cb][1]), pack_bf16x2(acc[cb][2], acc[cb][3])};
+                    *reinterpret_cast<u32x2*>(orow + cb * 16 + 4 * q4) = w2;
+                }
+            }
+            if (f + 1 < F) {
+#pragma unroll
+                for (int r = 0; r < 2; ++r) vr[r] = vn[r];
+#pragma unroll
+                for (int ks = 0; ks < 2; ++ks) {
+                    pr[ks][0] = pn[ks][0];
+                    pr[ks][1] = pn[ks][1];
+                }
             }
         }
     }
@@ -633,16 +847,36 @@ int persistent_grid(int64_t cap, int per_cu) {
     return static_cast<int>(cap < g ? (cap > 0 ? cap : 1) : g);
 }
 
+// Grid of the bf16 operators: at most four workgroups per CU, no more than the
+// items a plan of this capacity can hold (av_cap / H), and a multiple of
+// 8 * kOpRun so the XCD dealing is a permutation.
+int op_grid(const PlanView& p, int G) {
+    constexpr int64_t kUnit = 8 * kOpRun;
+    const int64_t items = std::max<int64_t>((p.av_cap + G - 1) / G, 1);
+    const int64_t g = std::min<int64_t>(items, (int64_t)device_cu_count() * 4);
+    return static_cast<int>((g + kUnit - 1) / kUnit * kUnit);
+}
+
+// Heads per item: the largest divisor of H that still leaves a plan of this
+// capacity (av_cap / G items at most) enough items to fill the GPU.
+int op_heads(const PlanView& p) {
+    const int64_t want = (int64_t)device_cu_count() * 4;
+    for (int G = p.heads; G > 1; --G)
+        if (p.heads % G == 0 && p.av_cap / G >= want) return G;
+    return 1;
+}
+
 }  // namespace
 
 hipError_t launch_qkt(const PlanView& p, int dtype, const void* q, int ldq, const void* k, int ldk, float scale,
                       void* scores, int64_t score_cap, bool causal, hipStream_t s) {
     const PlanArgs pa = plan_args(p);
-    const int grid = persistent_grid(dtype == 1 ? p.av_cap : p.qkt_cap, 8);
+    const int G = op_heads(p);
+    const int grid = dtype == 1 ? op_grid(p, G) : persistent_grid(p.qkt_cap, 8);
     if (dtype == 1)
         hipLaunchKernelGGL(k_qkt_bf16, dim3(grid), dim3(256), 0, s, pa, static_cast<const uint16_t*>(q), ldq,
                            static_cast<const uint16_t*>(k), ldk, scale, static_cast<uint16_t*>(scores), score_cap,
-                           int(causal));
+                           int(causal), G);
     else
         hipLaunchKernelGGL(k_qkt_f32, dim3(grid), dim3(256), 0, s, pa, static_cast<const float*>(q), ldq,
                            static_cast<const float*>(k), ldk, scale, static_cast<float*>(scores), score_cap,
@@ -667,10 +901,12 @@ hipError_t launch_softmax(const PlanView& p, int dtype, const void* scores, void
 hipError_t launch_attn_v(const PlanView& p, int dtype, const void* probs, int64_t score_cap, const void* v, int ldv,
                          void* out, int ldo, bool causal, hipStream_t s) {
     const PlanArgs pa = plan_args(p);
-    const int grid = persistent_grid(p.av_cap, 8);
+    const int G = op_heads(p);
+    const int grid = dtype == 1 ? op_grid(p, G) : persistent_grid(p.av_cap, 8);
     if (dtype == 1)
         hipLaunchKernelGGL(k_attn_v_bf16, dim3(grid), dim3(256), 0, s, pa, static_cast<const uint16_t*>(probs),
-                           score_cap, static_cast<const uint16_t*>(v), ldv, static_cast<uint16_t*>(out), ldo, int(causal));
+                           score_cap, static_cast<const uint16_t*>(v), ldv, static_cast<uint16_t*>(out), ldo, int(causal),
+                           G);
     else
         hipLaunchKernelGGL(k_attn_v_f32, dim3(grid), dim3(256), 0, s, pa, static_cast<const float*>(probs),
                            score_cap, static_cast<const float*>(v), ldv, static_cast<float*>(out), ldo, int(causal));
