@@ -214,6 +214,8 @@ rag_status softmax_impl(const rag_plan* plan, const void* scores, void* probs, i
     rag_status st;
     if ((st = view_plan(plan, v, fn)) || (st = check_dtype(dtype, fn))) return st;
     if (!scores || !probs || score_cap < 0) return fail(RAG_ERR_ARG, "%s: scores/probs NULL or score_cap < 0", fn);
+    if (dtype == RAG_BF16 && (int64_t)plan->heads * plan->max_len * 2 + 64 > INT32_MAX)
+        return fail(RAG_ERR_SHAPE, "%s: heads * max_len * 2 bytes exceeds 32-bit row offsets", fn);
     if (!aligned(scores, elem_size(dtype)) || !aligned(probs, elem_size(dtype)))
         return fail(RAG_ERR_ARG, "%s: scores/probs misaligned", fn);
     hipStream_t s = static_cast<hipStream_t>(stream);

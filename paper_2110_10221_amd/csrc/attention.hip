@@ -328,6 +328,65 @@ struct Elem<false> {
 
 constexpr int kSoftmaxRegs = 8;  // rows up to 64 * 8 = 512 scores stay in registers
 
+// One bf16 score row of n values starting at element E (any alignment) with R
+// aligned 16-byte chunks per lane (n + 7 <= 512 R): loads through the
+// range-checked descriptor rs (based at element e_base, a multiple of 8), an
+// exact max and sum over the row, whole chunks stored with 16-byte stores and
+// the partial chunks at both ends element by element (their other elements
+// belong to the neighbouring rows, so a whole-chunk store could race with them).
+template <int R>
+__device__ __forceinline__ void softmax_row_chunks(__amdgpu_buffer_rsrc_t rs, int64_t e_base, int64_t E, int n,
+                                                   uint16_t* P, int lane) {
+    const int64_t c0 = E >> 3;        // first chunk of the row
+    const int sh = (int)(E & 7);      // the row's first element within it
+    const int nch = (sh + n + 7) >> 3;
+    float x[R][8];
+    float m = -FLT_MAX;
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+        const int c = lane + kWave * r;
+        u32x4 raw = {0u, 0u, 0u, 0u};
+        if (c < nch)
+            raw = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rs, (int)((c0 + c) * 8 - e_base) * 2, 0, 0));
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+            const int j = 8 * c + e - sh;
+            const uint32_t w = raw[e >> 1];
+            const float v = __uint_as_float((e & 1) ? (w & 0xffff0000u) : (w << 16));
+            x[r][e] = (j >= 0 && j < n) ? v : -FLT_MAX;
+            m = fmaxf(m, x[r][e]);
+        }
+    }
+    m = wave_max(m);
+    float sum = 0.f;
+#pragma unroll
+    for (int r = 0; r < R; ++r)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+            const int j = 8 * (lane + kWave * r) + e - sh;
+            x[r][e] = (j >= 0 && j < n) ? __expf(x[r][e] - m) : 0.f;
+            sum += x[r][e];
+        }
+    const float inv = 1.0f / wave_sum(sum);
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+        const int c = lane + kWave * r;
+        if (c >= nch) continue;
+        const int j0 = 8 * c - sh;  // row position of the chunk's first element
+        uint16_t* dst = P + (c0 + c) * 8;
+        if (j0 >= 0 && j0 + 8 <= n) {
+            u32x4 o;
+#pragma unroll
+            for (int d = 0; d < 4; ++d) o[d] = pack_bf16x2(x[r][2 * d] * inv, x[r][2 * d + 1] * inv);
+            *reinterpret_cast<u32x4*>(dst) = o;
+        } else {
+#pragma unroll
+            for (int e = 0; e < 8; ++e)
+                if (j0 + e >= 0 && j0 + e < n) dst[e] = f32_to_bf16(x[r][e] * inv);
+        }
+    }
+}
+
 template <bool BF16>
 __global__ __launch_bounds__(256) void k_softmax(PlanArgs pa, const typename Elem<BF16>::T* S,
                                                   typename Elem<BF16>::T* P, int64_t score_cap, int T, int causal) {
@@ -356,6 +415,19 @@ __global__ __launch_bounds__(256) void k_softmax(PlanArgs pa, const typename Ele
             const float ex = valid ? E::exp(x - m) : 0.f;
             const float s = group_sum(ex, G);
             if (valid) E::store(P + off, ex * (1.0f / s));
+        }
+    } else if (BF16 && L + 7 <= 8 * kWave * 2) {
+        // aligned 16-byte chunks: the token's rows are one span of H * ld scores
+        const int64_t e_base = row0 & ~(int64_t)7;
+        const int64_t span_end = min(score_cap, row0 + (int64_t)(H - 1) * ld + L);
+        const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+            const_cast<void*>(static_cast<const void*>(S + e_base)), 0,
+            (uint32_t)min<int64_t>(((span_end - e_base) * 2 + 3) & ~(int64_t)3, (int64_t)0x7ffffffc), 0x00020000);
+        uint16_t* const Pb = reinterpret_cast<uint16_t*>(P);
+        if (L + 7 <= 8 * kWave) {
+            for (int h = 0; h < H; ++h) softmax_row_chunks<1>(rs, e_base, row0 + (int64_t)h * ld, L, Pb, lane);
+        } else {
+            for (int h = 0; h < H; ++h) softmax_row_chunks<2>(rs, e_base, row0 + (int64_t)h * ld, L, Pb, lane);
         }
     } else if (L <= kWave * kSoftmaxRegs) {
         for (int h = 0; h < H; ++h) {
