@@ -6,7 +6,10 @@ Parity criteria (from the required tolerances):
         operator; for the composed encoder layer the relative term is taken
         against the token row's scale, |gpu - oracle| <= 1e-3 + 2e-2 * max_row |oracle|
         (LayerNorm re-centres each row, so a one-ulp rounding flip upstream
-        lands as an absolute error on outputs that happen to be near zero)
+        lands as an absolute error on outputs that happen to be near zero;
+        tests/test_tolerance_readings.py shows an independent fp32 pipeline
+        doing the same), and each row's mean |gpu - oracle| / max_row |oracle|
+        at most ROW_MEAN_TOL
   fp32  per stored row r: max_i |gpu - oracle| <= 1e-5 * max_i |oracle|
         (row-normwise, so entries that cancel to near zero do not dominate)
   integers: exact equality
@@ -55,18 +58,36 @@ def bf16_close(got_bits: np.ndarray, ref_bits: np.ndarray):
     return bool(worst <= 0 and not bad.any()), worst
 
 
-def bf16_row_close(got_bits: np.ndarray, ref_bits: np.ndarray, row_len: int):
-    """(ok, worst excess) for the composed layer: per token row,
-    |g - o| <= 1e-3 + 2e-2 * max_row |o| element-wise."""
+ROW_MEAN_TOL = 1e-3  # per token row: mean |g - o| / max_row |o|
+ELEM_PASS_MIN = 0.98  # composed layer: fraction of elements within the element-wise bound
+
+
+def bf16_row_stats(got_bits: np.ndarray, ref_bits: np.ndarray, row_len: int) -> dict:
+    """Error statistics of a composed-layer output, per token row: the worst
+    excess over the row-scaled bound, the worst row mean of |g - o| / max_row |o|,
+    the worst excess over the element-wise bound and the fraction of elements
+    within it."""
     g = values(got_bits, "bf16").reshape(-1, row_len)
     o = values(ref_bits, "bf16").reshape(-1, row_len)
     if g.size == 0:
-        return True, 0.0
-    if not np.all(np.isfinite(g)):
+        return {"row_excess": 0.0, "row_mean": 0.0, "elem_excess": 0.0, "elem_pass": 1.0, "finite": True}
+    finite = bool(np.all(np.isfinite(g)))
+    err = np.abs(g - o)
+    rowmax = np.maximum(np.abs(o).max(axis=1, keepdims=True), 1e-30)
+    elem = err - (BF16_ATOL + BF16_RTOL * np.abs(o))
+    return {"row_excess": float((err - (BF16_ATOL + BF16_RTOL * rowmax)).max()),
+            "row_mean": float((err / rowmax).mean(axis=1).max()),
+            "elem_excess": float(elem.max()), "elem_pass": float((elem <= 0).mean()), "finite": finite}
+
+
+def bf16_row_close(got_bits: np.ndarray, ref_bits: np.ndarray, row_len: int):
+    """(ok, worst excess) for the composed layer: per token row,
+    |g - o| <= 1e-3 + 2e-2 * max_row |o| element-wise, and the row's mean
+    |g - o| / max_row |o| at most ROW_MEAN_TOL (rounding-level on average)."""
+    st = bf16_row_stats(got_bits, ref_bits, row_len)
+    if not st["finite"]:
         return False, float("inf")
-    excess = np.abs(g - o) - (BF16_ATOL + BF16_RTOL * np.abs(o).max(axis=1, keepdims=True))
-    worst = float(excess.max())
-    return worst <= 0, worst
+    return st["row_excess"] <= 0 and st["row_mean"] <= ROW_MEAN_TOL, st["row_excess"]
 
 
 def rowwise_close(got: np.ndarray, ref: np.ndarray, rtol: float = F32_RTOL, row_len: int | None = None) -> bool:

@@ -10,7 +10,7 @@ import pytest
 import torch
 
 import oracle
-from tests.helpers import bf16_close, bf16_row_close, canary_buffer, canary_intact, close, dev, host
+from tests.helpers import ELEM_PASS_MIN, bf16_row_close, bf16_row_stats, canary_buffer, canary_intact, close, dev, host
 from workloads import WEIGHT_NAMES, BIAS_NAMES, LN_NAMES, make_workload, random_storage
 
 pytestmark = pytest.mark.gpu
@@ -63,35 +63,84 @@ def test_small_layers(dtype, flags, L):
         assert close(got, ref, "f32", d)
 
 
-def _sample_check(wl, got, picks):
+def _sample_check(wl, got, picks, causal=False):
+    """Each picked sequence against the oracle (a sequence's outputs depend on its
+    own tokens only); the oracle runs the sequences in parallel threads."""
+    from concurrent.futures import ThreadPoolExecutor
+
     cfg = wl.cfg
     L = wl.lengths
     st = np.concatenate([[0], np.cumsum(L)])
     w = {n: wl.tensors[n] for n in WEIGHT_NAMES + BIAS_NAMES + LN_NAMES}
-    for b in picks:
-        print(f"  oracle sequence {b} (L={L[b]})", flush=True)
+
+    def ref(b):
         xs = wl.tensors["x"][st[b]:st[b + 1]]
-        ref = oracle.encoder_layer("bf16", L[b:b + 1], xs, w, cfg.d_model, cfg.heads, cfg.d_ff)
-        ok, worst = bf16_row_close(got[st[b]:st[b + 1]], ref, cfg.d_model)
-        elem_ok, elem_worst = bf16_close(got[st[b]:st[b + 1]], ref)
-        print(f"    row-scaled worst excess {worst:.2e}; element-wise worst excess {elem_worst:.2e}", flush=True)
-        assert ok, (b, int(L[b]), worst)
+        return oracle.encoder_layer("bf16", L[b:b + 1], xs, w, cfg.d_model, cfg.heads, cfg.d_ff, causal=causal)
+
+    print(f"  oracle on {len(picks)} sequences ({int(sum(L[b] for b in picks))} tokens)", flush=True)
+    with ThreadPoolExecutor(max_workers=min(16, len(picks))) as ex:
+        refs = list(ex.map(ref, picks))
+    worst = {"row_excess": -np.inf, "row_mean": 0.0, "elem_excess": -np.inf, "elem_pass": 1.0}
+    for b, r in zip(picks, refs):
+        stats = bf16_row_stats(got[st[b]:st[b + 1]], r, cfg.d_model)
+        ok, _ = bf16_row_close(got[st[b]:st[b + 1]], r, cfg.d_model)
+        assert ok, (b, int(L[b]), stats)
+        for key in ("row_excess", "row_mean", "elem_excess"):
+            worst[key] = max(worst[key], stats[key])
+        worst["elem_pass"] = min(worst["elem_pass"], stats["elem_pass"])
+    print(f"    worst: row-scaled excess {worst['row_excess']:.2e}, row mean |err|/rowmax {worst['row_mean']:.2e}, "
+          f"element-wise excess {worst['elem_excess']:.2e}, element-wise pass fraction {worst['elem_pass']:.5f}",
+          flush=True)
+    # the element-wise bound holds for all but a few elements near zero (rounding
+    # flips; an emulation of the kernels' arithmetic shows the same fraction)
+    assert worst["elem_pass"] >= ELEM_PASS_MIN, worst
+    return worst
 
 
-@pytest.mark.parametrize("cid,flags", [(3, 0), (3, 1), (5, 0), (4, 0)])
+def _spread_picks(L, n):
+    """n sequences spread over the caller order (their tokens reach GEMM tiles
+    throughout the batch), plus the longest, the shortest and the last."""
+    order = np.argsort(-L, kind="stable")
+    picks = set(np.linspace(0, len(L) - 1, n).round().astype(int).tolist())
+    picks |= {int(order[0]), int(order[-1]), len(L) - 1}
+    return sorted(picks)
+
+
+@pytest.mark.parametrize("cid,flags", [(3, 0), (3, 1), (5, 0)])
 def test_benchmark_configs_sampled_sequences(cid, flags):
     wl = make_workload(cid, seed=0, random_ln=True)
     cfg = wl.cfg
     print(f"layer config {cid} flags {flags}: B={cfg.batch} T={wl.total_tokens}", flush=True)
     w = {n: wl.tensors[n] for n in WEIGHT_NAMES + BIAS_NAMES + LN_NAMES}
     got = _gpu_layer(wl.lengths, wl.tensors["x"], w, cfg.d_model, cfg.heads, cfg.d_ff, "bf16", flags)
+    _sample_check(wl, got, _spread_picks(wl.lengths, 8))
+
+
+@pytest.mark.parametrize("causal", [False, True])
+def test_batch128_layer_as_benchmarked(causal):
+    # the benchmark's exact call: the batch-128 d1024 layer building its own plan
+    # (the prelude inside the QKV projection's launch), fused attention; the
+    # oracle checks 16 sequences spread over the batch, the longest, the
+    # shortest and the last (whose tokens fill the GEMMs' last tile rows)
+    import paper_2110_10221_amd as rag
+
+    wl = make_workload(4, seed=0, random_ln=True)
+    cfg = wl.cfg
     L = wl.lengths
-    order = np.argsort(-L, kind="stable")
-    # the longest, the shortest and two in between, and the last in caller order
-    # (its tokens fall in the GEMMs' last tile rows, where a sparse last round of
-    # tiles runs as 64-token halves)
-    picks = sorted({int(order[0]), int(order[-1]), int(order[len(L) // 2]), int(order[len(L) // 3]), len(L) - 1})
-    _sample_check(wl, got, picks)
+    T, d = wl.total_tokens, cfg.d_model
+    print(f"batch-128 layer causal={causal}: T={T}", flush=True)
+    flags = rag.RAG_LAYER_BUILD_PLAN | (rag.RAG_LAYER_CAUSAL if causal else 0)
+    plan = rag.Plan(torch.from_numpy(L).cuda(), T, cfg.max_len, cfg.heads)
+    wd = {n: dev(wl.tensors[n], "bf16") for n in WEIGHT_NAMES + BIAS_NAMES + LN_NAMES}
+    ws = torch.empty(rag.encoder_layer_workspace(T, cfg.max_len, d, cfg.heads, cfg.d_ff, rag.RAG_BF16, flags),
+                     dtype=torch.uint8, device="cuda")
+    whole, y = canary_buffer(T * d, "bf16")
+    rag.encoder_layer(plan, dev(wl.tensors["x"], "bf16"), y.view(T, d), wd, cfg.d_ff, ws, flags=flags)
+    torch.cuda.synchronize()
+    assert not plan.data_errors(), plan.data_errors()
+    assert canary_intact(whole, T * d)
+    got = host(y, "bf16").reshape(T, d)
+    _sample_check(wl, got, _spread_picks(L, 16), causal=causal)
 
 
 def test_layer_permutation_equivariance_and_determinism():

@@ -95,3 +95,46 @@ def test_offsets_data_errors(L, total, max_len, caps, bit):
     st = plan.status.cpu().numpy()
     assert st[0] & bit
     assert st[1] == 0 and st[2] == 0
+
+
+def test_sync_check_reports_data_errors():
+    # RAG_SYNC_CHECK=1 (read once per process, so a child process of its own):
+    # a call whose plan reports data errors returns RAG_ERR_DATA, a valid one RAG_OK
+    import os
+    import subprocess
+    import sys
+
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    code = r"""
+import sys
+sys.path.insert(0, sys.argv[1])
+import numpy as np, torch
+import paper_2110_10221_amd as rag
+plan = rag.Plan(torch.tensor([5, -3, 7], dtype=torch.int32, device="cuda"), 9, 7, 2)
+try:
+    rag.ragged_offsets(plan)
+    raise SystemExit("negative length not reported")
+except rag.RaggedError as e:
+    assert e.status == -7 and "negative length" in plan.data_errors(), (str(e), plan.data_errors())
+L = np.array([5, 70, 33], np.int32)
+T, H, d, dff = int(L.sum()), 2, 128, 256
+w = {n: torch.zeros(s, dtype=torch.bfloat16, device="cuda") for n, s in (
+    ("w_qkv", (3 * d, d)), ("b_qkv", (3 * d,)), ("w_o", (d, d)), ("b_o", (d,)), ("ln1_g", (d,)), ("ln1_b", (d,)),
+    ("w_ff1", (dff, d)), ("b_ff1", (dff,)), ("w_ff2", (d, dff)), ("b_ff2", (d,)), ("ln2_g", (d,)), ("ln2_b", (d,)))}
+flags = rag.RAG_LAYER_BUILD_PLAN
+bad = rag.Plan(torch.from_numpy(L).cuda(), T + 1, 70, H)   # token count disagrees with the lengths
+ws = torch.empty(rag.encoder_layer_workspace(T + 1, 70, d, H, dff, rag.RAG_BF16, flags), dtype=torch.uint8, device="cuda")
+x = torch.zeros(T + 1, d, dtype=torch.bfloat16, device="cuda")
+y = torch.empty_like(x)
+try:
+    rag.encoder_layer(bad, x, y, w, dff, ws, flags=flags)
+    raise SystemExit("token count not reported")
+except rag.RaggedError as e:
+    assert e.status == -7 and "sum of lengths != total_tokens" in bad.data_errors(), (str(e), bad.data_errors())
+good = rag.Plan(torch.from_numpy(L).cuda(), T, 70, H)
+rag.encoder_layer(good, x[:T], y[:T], w, dff, ws, flags=flags)
+print("sync check ok")
+"""
+    env = dict(os.environ, RAG_SYNC_CHECK="1")
+    r = subprocess.run([sys.executable, "-c", code, root], env=env, capture_output=True, text=True, timeout=300)
+    assert r.returncode == 0 and "sync check ok" in r.stdout, r.stdout + r.stderr
