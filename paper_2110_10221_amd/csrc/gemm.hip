@@ -31,9 +31,12 @@
 //        faster on the layer's GEMMs).
 //      ring (trmm): three stages of 32 k, copies issued three steps ahead, 72 KB.
 //  - The MFMA computes the transposed tile C[n][m] = sum_k w[n][k] x[m][k], so each
-//    lane ends with four consecutive output features of one token.  The fp32
-//    results pass through LDS in 32-token slices so that bias / activation /
-//    residual are applied while whole 512-byte rows move to and from memory.
+//    lane ends with four consecutive output features of one token.  Results pass
+//    through LDS so that whole 512-byte rows move to memory: without a residual,
+//    bias and activation are applied to the accumulators and the whole tile is
+//    staged as bf16 rows at once (one barrier pair); with a residual, fp32
+//    results are staged in 32-token slices and bias / activation / residual are
+//    applied in the row phase, so the sum is rounded once.
 //
 // The same tile body (gemm_tile_bf16) also serves the variable-sized batched
 // GEMM (one workgroup per entry of a plan's tile list, Section 7.1) and the
@@ -465,6 +468,52 @@ __device__ __forceinline__ void gemm_tile_bf16(const uint16_t* __restrict__ x, i
     step_last(fa1, fb1);
     }
 
+    if constexpr (!HAS_RES && !W_KN && !TRI) {
+        // no residual: bias and activation on the accumulators, bf16 rows staged in
+        // LDS all at once (BM rows of 512 bytes, 16-byte chunk c of row r at
+        // physical chunk c ^ (r & 31)), then whole rows stored
+        uint32_t* eb = reinterpret_cast<uint32_t*>(smem);
+        barrier_lds();  // the K loop is done with LDS
+#pragma unroll
+        for (int i = 0; i < FN; ++i)
+#pragma unroll
+            for (int g = 0; g < 4; ++g) {
+                const int f0 = wn * WN + i * 32 + 8 * g + 4 * h2;  // feature (in the tile) of acc[.][.][4g]
+                float bv[4] = {0.f, 0.f, 0.f, 0.f};
+                if constexpr (HAS_BIAS) {
+                    if (n0 + f0 < N) {
+                        const u32x2 bb = *reinterpret_cast<const u32x2*>(bias + n0 + f0);
+                        bv[0] = lo_bf16(bb[0]);
+                        bv[1] = hi_bf16(bb[0]);
+                        bv[2] = lo_bf16(bb[1]);
+                        bv[3] = hi_bf16(bb[1]);
+                    }
+                }
+#pragma unroll
+                for (int j = 0; j < FM; ++j) {
+                    const int r = j * 32 + l32;
+                    float v[4];
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) v[e] = activate_bf16<ACT>(acc[i][j][4 * g + e] + bv[e]);
+                    const int pc = (f0 >> 3) ^ (r & 31);
+                    *reinterpret_cast<u32x2*>(eb + r * 128 + pc * 4 + h2 * 2) =
+                        u32x2{pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3])};
+                }
+            }
+        barrier_lds();
+        // each wave instruction stores two 512-byte rows: lane / 32 picks the row, lane % 32 its chunk
+        const int cl = lane % 32;
+        const int n = n0 + 8 * cl;
+#pragma unroll
+        for (int rr = 0; rr < BM / 8; ++rr) {
+            const int r = (rr * C::kWaves + wave) * 2 + h2;
+            const int m = m0 + r;
+            if (m < T && n < N)
+                *reinterpret_cast<u32x4*>(y + (int64_t)m * ldy + n) =
+                    *reinterpret_cast<const u32x4*>(eb + r * 128 + ((cl ^ (r & 31)) * 4));
+        }
+        return;
+    }
     // Epilogue through LDS, 32 tokens at a time: the waves holding a slice write
     // their fp32 accumulators there, then all waves read whole rows back (16 bytes
     // per lane, 256 features per row), apply bias, activation and residual and
