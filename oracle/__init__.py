@@ -26,14 +26,19 @@ ACT_NONE, ACT_GELU_ERF, ACT_GELU_TANH = 0, 1, 2
 _DT = {"f32": F32, "bf16": BF16, F32: F32, BF16: BF16}
 
 
-def build(force: bool = True) -> str:
+SANITIZE_CC = "/opt/rocm/llvm/bin/clang"  # the compiler of the sanitizer runtime libragged's host code uses
+
+
+def build(force: bool = True, sanitize: bool = False) -> str:
     """Compile oracle.c into liboracle.so with gcc (strict IEEE: no fast-math,
-    no FMA contraction)."""
+    no FMA contraction).  `sanitize` builds it with AddressSanitizer and
+    UndefinedBehaviorSanitizer instead (clang, whose runtime must then be
+    preloaded into the Python process)."""
     if force or not os.path.exists(_LIB):
         tmp = _LIB + ".tmp"
-        subprocess.check_call([
-            "gcc", "-O2", "-std=gnu11", "-fPIC", "-shared", "-ffp-contract=off",
-            "-fno-fast-math", "-Wall", "-o", tmp, _SRC, "-lm"])
+        cc = [SANITIZE_CC, "-fsanitize=address,undefined", "-fno-omit-frame-pointer", "-g"] if sanitize else ["gcc"]
+        subprocess.check_call(cc + ["-O2", "-std=gnu11", "-fPIC", "-shared", "-ffp-contract=off",
+                                    "-fno-fast-math", "-Wall", "-o", tmp, _SRC, "-lm"])
         os.replace(tmp, _LIB)
     return _LIB
 

@@ -24,6 +24,9 @@ COMMON = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}", "-I", INCLUDE,
           "-Wall", "-Wno-unused-function"]
 # packed fp32 instructions stay off for all device code
 DEVICE = ["-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
+# host-side AddressSanitizer + UndefinedBehaviorSanitizer (device code unchanged)
+SANITIZE = ["-Xarch_host", "-fsanitize=address", "-Xarch_host", "-fsanitize=undefined",
+            "-Xarch_host", "-fno-omit-frame-pointer", "-g"]
 
 
 def hipcc() -> str:
@@ -33,25 +36,31 @@ def hipcc() -> str:
     raise RuntimeError("hipcc not found (ROCm is required to build the HIP library)")
 
 
-def _compile(src: str, defines=(), obj_dir: str = OBJ_DIR) -> str:
+def _compile(src: str, defines=(), obj_dir: str = OBJ_DIR, sanitize: bool = False) -> str:
     path = os.path.join(CSRC, src)
     obj = os.path.join(obj_dir, src + ".o")
-    cmd = [hipcc()] + COMMON + list(defines) + (DEVICE if src.endswith(".hip") else []) + ["-c", path, "-o", obj]
+    cmd = ([hipcc()] + COMMON + list(defines) + (DEVICE if src.endswith(".hip") else []) +
+           (SANITIZE if sanitize else []) + ["-c", path, "-o", obj])
     res = subprocess.run(cmd, capture_output=True, text=True)
     if res.returncode != 0:
         raise RuntimeError(f"compiling {src} failed:\n{' '.join(cmd)}\n{res.stdout}\n{res.stderr}")
     return obj
 
 
-def build(jobs: int | None = None, out: str = LIB, defines=()) -> str:
-    """Compile and link; `out` and `defines` (extra -D flags) serve alternate builds."""
-    obj_dir = OBJ_DIR if out == LIB else os.path.join(OBJ_DIR, os.path.basename(out) + ".objs")
+def build(jobs: int | None = None, out: str = LIB, defines=(), sanitize: bool = False) -> str:
+    """Compile and link; `out` and `defines` (extra -D flags) serve alternate builds;
+    `sanitize` instruments the host code with AddressSanitizer and
+    UndefinedBehaviorSanitizer (the loading process must preload clang's ASan
+    runtime; CPU checks only)."""
+    obj_dir = os.path.join(OBJ_DIR, "sanitize") if sanitize else OBJ_DIR
+    if out != LIB:
+        obj_dir = os.path.join(obj_dir, os.path.basename(out) + ".objs")
     os.makedirs(obj_dir, exist_ok=True)
     jobs = jobs or min(len(SOURCES), os.cpu_count() or 4)
     with concurrent.futures.ThreadPoolExecutor(jobs) as ex:
-        objs = list(ex.map(lambda src: _compile(src, defines, obj_dir), SOURCES))
+        objs = list(ex.map(lambda src: _compile(src, defines, obj_dir, sanitize), SOURCES))
     tmp = out + ".tmp"
-    cmd = [hipcc(), "-shared", "-fPIC", f"--offload-arch={ARCH}", "-o", tmp] + objs
+    cmd = [hipcc(), "-shared", "-fPIC", f"--offload-arch={ARCH}", "-o", tmp] + (SANITIZE if sanitize else []) + objs
     res = subprocess.run(cmd, capture_output=True, text=True)
     if res.returncode != 0:
         raise RuntimeError(f"linking failed:\n{' '.join(cmd)}\n{res.stdout}\n{res.stderr}")
@@ -65,5 +74,6 @@ if __name__ == "__main__":
     ap = argparse.ArgumentParser()
     ap.add_argument("--out", default=LIB)
     ap.add_argument("-D", dest="defines", action="append", default=[])
+    ap.add_argument("--sanitize", action="store_true", help="host-side ASan + UBSan build (CPU checks)")
     a = ap.parse_args()
-    print(build(out=os.path.abspath(a.out), defines=[f"-D{d}" for d in a.defines]))
+    print(build(out=os.path.abspath(a.out), defines=[f"-D{d}" for d in a.defines], sanitize=a.sanitize))
