@@ -671,6 +671,144 @@ __global__ __launch_bounds__(256) void k_gemm_f32(const float* __restrict__ x, i
     gemm_tile_f32<ACT>(x, ldx, w, bias, residual, ldr, y, ldy, T, K, N, blockIdx.x * 64, blockIdx.y * 64);
 }
 
+// fp32 on the matrix cores: v_mfma_f32_32x32x2f32 (fp32 products and fp32
+// accumulation, as the VALU kernel above).  128 x 128 output tiles, four waves
+// of 64 x 64; operands go global -> LDS with bounds-checked buffer loads (rows
+// past T or N read as zeros) into two stages of 32 k, 128-byte rows whose
+// 16-byte chunks are XOR-swizzled like the bf16 paired-w rows.  In MFMA step s
+// of an 8-k group a lane supplies k = 4 (lane / 32) + s (the same k order for
+// both operands), so one 16-byte LDS read feeds four MFMAs.  The MFMA computes
+// C^T = W X^T: a lane holds four consecutive output features of one token,
+// stored as one 16-byte vector.
+constexpr int kF32M = 128, kF32N = 128, kF32K = 32;
+constexpr int kF32StageFloats = (kF32M + kF32N) * kF32K;
+constexpr int kF32Lds = 2 * kF32StageFloats * 4;
+
+template <int ACT, bool HB, bool HR>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2)))
+void k_gemm_f32_mfma(const float* __restrict__ x, int ldx, const float* __restrict__ w,
+                     const float* __restrict__ bias, const float* residual, int ldr, float* y, int ldy, int T,
+                     int K, int N, int tiles_m, int tiles_n) {
+    extern __shared__ __attribute__((aligned(16))) float fsm[];
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave), lane = threadIdx.x % kWave;
+    const int l32 = lane % 32, h2 = lane / 32;
+    const int wm = wave >> 1, wn = wave & 1;  // the wave's 64 tokens and 64 features
+    int tm, tn;
+    tile_coords(blockIdx.x, gridDim.x, tiles_m, tiles_n, tm, tn);
+    const int m0 = tm * kF32M, n0 = tn * kF32N;
+    const __amdgpu_buffer_rsrc_t rx = make_rsrc(x + (int64_t)m0 * ldx, (uint32_t)min(T - m0, kF32M) * ldx * 4u);
+    const __amdgpu_buffer_rsrc_t rw = make_rsrc(w + (int64_t)n0 * K, (uint32_t)min(N - n0, kF32N) * K * 4u);
+    // copy block b (1 KB: 8 rows of 128 bytes; blocks 0-15 x rows, 16-31 w rows):
+    // this wave fills blocks 8 wave .. 8 wave + 7, lane l slot l (row 8 b' + l / 8,
+    // physical chunk l % 8, which holds logical chunk (l % 8) ^ swz2(row))
+    int voff[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+        const int blk = wave * 8 + i, bl = blk & 15, row = bl * 8 + lane / 8;
+        voff[i] = row * (blk < 16 ? ldx : K) * 4 + ((lane % 8) ^ swz2(row)) * 16;
+    }
+    auto issue = [&](int step) {
+        float* st = fsm + (step & 1) * kF32StageFloats;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            const int blk = wave * 8 + i;
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(blk < 16 ? rx : rw, (lds_void_t*)(st + blk * 256), 16, voff[i],
+                                                     step * kF32K * 4, 0, 0);
+        }
+    };
+    floatx16 acc[2][2];
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+    const int nk = K / kF32K;
+    issue(0);
+    for (int k = 0; k < nk; ++k) {
+        wait_vm<0>();
+        barrier_lds();  // step k's stage is visible; the other stage is no longer read
+        if (k + 1 < nk) issue(k + 1);
+        const float* xs = fsm + (k & 1) * kF32StageFloats;
+        const float* ws = xs + kF32M * kF32K;
+#pragma unroll
+        for (int gq = 0; gq < 4; ++gq) {
+            floatx4 a[2], bq[2];
+#pragma unroll
+            for (int i = 0; i < 2; ++i) {
+                const int r = wn * 64 + i * 32 + l32;
+                a[i] = *reinterpret_cast<const floatx4*>(ws + r * kF32K + (((gq * 2 + h2) ^ swz2(r)) * 4));
+            }
+#pragma unroll
+            for (int j = 0; j < 2; ++j) {
+                const int r = wm * 64 + j * 32 + l32;
+                bq[j] = *reinterpret_cast<const floatx4*>(xs + r * kF32K + (((gq * 2 + h2) ^ swz2(r)) * 4));
+            }
+#pragma unroll
+            for (int st = 0; st < 4; ++st)
+#pragma unroll
+                for (int i = 0; i < 2; ++i)
+#pragma unroll
+                    for (int j = 0; j < 2; ++j)
+                        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[i][st], bq[j][st], acc[i][j], 0, 0, 0);
+        }
+    }
+    // acc[i][j][4g + r]: token wm*64 + j*32 + l32, feature wn*64 + i*32 + 8g + 4 h2 + r
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+            const int n = n0 + wn * 64 + i * 32 + 8 * g + 4 * h2;
+            if (n >= N) continue;
+            floatx4 bv = {0.f, 0.f, 0.f, 0.f};
+            if constexpr (HB) bv = *reinterpret_cast<const floatx4*>(bias + n);
+#pragma unroll
+            for (int j = 0; j < 2; ++j) {
+                const int m = m0 + wm * 64 + j * 32 + l32;
+                if (m >= T) continue;
+                floatx4 o;
+#pragma unroll
+                for (int r = 0; r < 4; ++r) o[r] = activate<ACT>(acc[i][j][4 * g + r] + bv[r]);
+                if constexpr (HR) o += *reinterpret_cast<const floatx4*>(residual + (int64_t)m * ldr + n);
+                *reinterpret_cast<floatx4*>(y + (int64_t)m * ldy + n) = o;
+            }
+        }
+}
+
+template <int ACT, bool HB, bool HR>
+hipError_t launch_f32_mfma(const float* x, int ldx, const float* w, const float* bias, const float* residual, int ldr,
+                           float* y, int ldy, int T, int K, int N, hipStream_t s) {
+    static bool attr_set = false;  // benign race: every thread sets the same value
+    if (!attr_set) {
+        hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_gemm_f32_mfma<ACT, HB, HR>),
+                                           hipFuncAttributeMaxDynamicSharedMemorySize, kF32Lds);
+        if (e != hipSuccess) return e;
+        attr_set = true;
+    }
+    const int tiles_m = (T + kF32M - 1) / kF32M, tiles_n = (N + kF32N - 1) / kF32N;
+    hipLaunchKernelGGL((k_gemm_f32_mfma<ACT, HB, HR>), dim3(tiles_m * tiles_n), dim3(256), kF32Lds, s, x, ldx, w, bias,
+                       residual, ldr, y, ldy, T, K, N, tiles_m, tiles_n);
+    return hipGetLastError();
+}
+
+template <int ACT>
+hipError_t launch_f32_mfma_act(const float* x, int ldx, const float* w, const float* bias, const float* residual,
+                               int ldr, float* y, int ldy, int T, int K, int N, hipStream_t s) {
+    if (bias && residual) return launch_f32_mfma<ACT, true, true>(x, ldx, w, bias, residual, ldr, y, ldy, T, K, N, s);
+    if (bias) return launch_f32_mfma<ACT, true, false>(x, ldx, w, bias, residual, ldr, y, ldy, T, K, N, s);
+    if (residual) return launch_f32_mfma<ACT, false, true>(x, ldx, w, bias, residual, ldr, y, ldy, T, K, N, s);
+    return launch_f32_mfma<ACT, false, false>(x, ldx, w, bias, residual, ldr, y, ldy, T, K, N, s);
+}
+
+// The matrix-core fp32 kernel needs whole 32-k steps, 16-byte vectors (rows of x,
+// w, y and residual and the bias 16-byte aligned) and N % 4 == 0.
+bool f32_mfma_ok(const void* x, int ldx, const void* w, const void* bias, const void* residual, int ldr,
+                 const void* y, int ldy, int K, int N) {
+    auto al = [](const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; };
+    return K % kF32K == 0 && N % 4 == 0 && ldx % 4 == 0 && ldy % 4 == 0 && al(x) && al(w) && al(y) &&
+           (!bias || al(bias)) && (!residual || (al(residual) && ldr % 4 == 0));
+}
+
 // ---------------------------------------------------------------------------
 // Variable-sized batched GEMM: one workgroup per entry of the plan's tile list
 // (problems largest first).  The workgroup -> entry map deals the list to the
@@ -976,6 +1114,11 @@ hipError_t launch_linear(int dtype, const void* x, int ldx, const void* w, const
     const float* bf = static_cast<const float*>(bias);
     const float* rf = static_cast<const float*>(residual);
     float* yf = static_cast<float*>(y);
+    if (f32_mfma_ok(x, ldx, w, bias, residual, ldr, y, ldy, K, N)) {
+        if (act == 1) return launch_f32_mfma_act<1>(xf, ldx, wf, bf, rf, ldr, yf, ldy, T, K, N, s);
+        if (act == 2) return launch_f32_mfma_act<2>(xf, ldx, wf, bf, rf, ldr, yf, ldy, T, K, N, s);
+        return launch_f32_mfma_act<0>(xf, ldx, wf, bf, rf, ldr, yf, ldy, T, K, N, s);
+    }
     if (act == 1) hipLaunchKernelGGL(k_gemm_f32<1>, grid, dim3(256), 0, s, xf, ldx, wf, bf, rf, ldr, yf, ldy, T, K, N);
     else if (act == 2) hipLaunchKernelGGL(k_gemm_f32<2>, grid, dim3(256), 0, s, xf, ldx, wf, bf, rf, ldr, yf, ldy, T, K, N);
     else hipLaunchKernelGGL(k_gemm_f32<0>, grid, dim3(256), 0, s, xf, ldx, wf, bf, rf, ldr, yf, ldy, T, K, N);
