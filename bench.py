@@ -30,6 +30,7 @@ sys.path.insert(0, ROOT)
 
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
+PEAK_F32_TFLOPS = 157.3     # MI355X dense fp32 MFMA
 METRIC = "ms/encoder layer + useful (unpadded) TFLOP/s, fraction of bf16 MFMA peak"
 
 # stage index (events[k] .. events[k+1]) -> kernel symbol
@@ -425,6 +426,21 @@ def other_configs_measurement(rag, iters=30):
                         "useful_tflops": round(uf / (ms * 1e-3) / 1e12, 1),
                         "frac_of_bf16_peak": round(uf / (ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
                         "padded_fraction": round(padded_fraction(L, d, dff), 4)})
+            if cid == 3:
+                # the same layer in fp32 (fp32 storage, products and accumulation; the
+                # operator attention chain), against the fp32 matrix peak
+                from workloads import bf16_bits_to_f32
+                xf = dev(bf16_bits_to_f32(wl.tensors["x"]), "f32")
+                wdf = {n: dev(bf16_bits_to_f32(wl.tensors[n]), "f32") for n in WEIGHT_NAMES + BIAS_NAMES + LN_NAMES}
+                wf = rag.layer_weights(wdf)  # wdf keeps the tensors alive
+                wsf = torch.empty(rag.encoder_layer_workspace(T, cfg.max_len, d, H, dff, rag.RAG_F32, 0),
+                                  dtype=torch.uint8, device="cuda")
+                yf = torch.empty(T, d, dtype=torch.float32, device="cuda")
+                msf = _timed(lambda: rag.encoder_layer(plan, xf, yf, wf, dff, wsf, flags=rag.RAG_LAYER_BUILD_PLAN),
+                             iters)
+                rec["fp32_layer"] = {"ms_per_layer": round(msf, 4),
+                                     "useful_tflops": round(uf / (msf * 1e-3) / 1e12, 2),
+                                     "frac_of_f32_peak": round(uf / (msf * 1e-3) / 1e12 / PEAK_F32_TFLOPS, 4)}
         assert not plan.data_errors(), plan.data_errors()
         out[f"config{cid}"] = rec
     return out

@@ -254,14 +254,25 @@ __global__ __launch_bounds__(256) void k_qkt_bf16(PlanArgs pa, const uint16_t* _
     }
 }
 
+// fp32 QK^T: one 64 x 64 score tile per item, Q and K rows staged in LDS; wave w
+// computes the 32 x 32 block (queries 32 (w / 2) .., keys 32 (w % 2) ..) on
+// v_mfma_f32_32x32x2f32 (fp32 products and accumulation).  A lane holds key
+// l % 32 of the block and queries 8 (r / 4) + 4 (l / 32) + r % 4, so each
+// accumulator register is stored as 32 consecutive floats of one score row.
+// Row stride 66 floats: the 64 lanes of an operand read (row l % 32, column
+// c + l / 32) fall in 64 distinct banks.
+constexpr int kF32Row = kHeadDim + 2;
+
 __global__ __launch_bounds__(256) void k_qkt_f32(PlanArgs pa, const float* __restrict__ q, int ldq,
                                                   const float* __restrict__ k, int ldk, float scale,
                                                   float* __restrict__ S, int64_t score_cap, int causal) {
     if (!plan_ok(pa, score_cap)) return;
-    __shared__ float Qs[kTile][kHeadDim + 1], Ks[kTile][kHeadDim + 1];
+    __shared__ float Qs[kTile][kF32Row], Ks[kTile][kF32Row];
     const int n_items = pa.status[1];
     const int H = pa.heads;
-    const int tx = threadIdx.x % 16, ty = threadIdx.x / 16;
+    const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
+    const int l32 = lane % 32, h2 = lane / 32;
+    const int wq = wave >> 1, wk = wave & 1;
     for (int it = blockIdx.x; it < n_items; it += gridDim.x) {
         const int4 item = reinterpret_cast<const int4*>(pa.qkt_items)[it];
         const int b = item.x, h = item.y, ti = item.z, tj = item.w;
@@ -277,29 +288,20 @@ __global__ __launch_bounds__(256) void k_qkt_f32(PlanArgs pa, const float* __res
             Ks[r][c] = k[(int64_t)(t0 + kj) * ldk + h * kHeadDim + c];
         }
         __syncthreads();
-        float acc[4][4] = {};
-        for (int c = 0; c < kHeadDim; ++c) {
-            float a[4], bb[4];
+        floatx16 acc;
 #pragma unroll
-            for (int u = 0; u < 4; ++u) {
-                a[u] = Qs[ty * 4 + u][c];
-                bb[u] = Ks[tx + 16 * u][c];
-            }
-#pragma unroll
-            for (int u = 0; u < 4; ++u)
-#pragma unroll
-                for (int v = 0; v < 4; ++v) acc[u][v] = fmaf(a[u], bb[v], acc[u][v]);
-        }
+        for (int r = 0; r < 16; ++r) acc[r] = 0.f;
+#pragma unroll 8
+        for (int c = 0; c < kHeadDim; c += 2)
+            acc = __builtin_amdgcn_mfma_f32_32x32x2f32(Qs[wq * 32 + l32][c + h2], Ks[wk * 32 + l32][c + h2], acc, 0, 0, 0);
         const int rows = min(kTile, L - ti * kTile), cols = min(kTile, L - tj * kTile);
+        const int j = wk * 32 + l32;
+        if (j < cols) {
 #pragma unroll
-        for (int u = 0; u < 4; ++u) {
-            const int i = ty * 4 + u;
-            if (i >= rows) continue;
-#pragma unroll
-            for (int v = 0; v < 4; ++v) {
-                const int j = tx + 16 * v;
-                if (j < cols && (!causal || tj * kTile + j <= ti * kTile + i))
-                    S[base + ((int64_t)(ti * kTile + i) * H + h) * L + tj * kTile + j] = acc[u][v] * scale;
+            for (int r = 0; r < 16; ++r) {
+                const int i = wq * 32 + 8 * (r / 4) + 4 * h2 + r % 4;
+                if (i < rows && (!causal || tj * kTile + j <= ti * kTile + i))
+                    S[base + ((int64_t)(ti * kTile + i) * H + h) * L + tj * kTile + j] = acc[r] * scale;
             }
         }
     }
@@ -615,21 +617,30 @@ __global__ __launch_bounds__(256) void k_attn_v_bf16(PlanArgs pa, const uint16_t
     }
 }
 
+// fp32 Attn.V: one 64-query block of one head per item, probabilities and V
+// staged in LDS 64 keys at a time; wave w accumulates the 32 x 32 block
+// (queries 32 (w / 2) .., channels 32 (w % 2) ..) on v_mfma_f32_32x32x2f32.  V's
+// row stride 96 puts the operand read (row kk + l / 32, column l % 32) in 64
+// distinct banks.
 __global__ __launch_bounds__(256) void k_attn_v_f32(PlanArgs pa, const float* __restrict__ P, int64_t score_cap,
                                                      const float* __restrict__ v, int ldv, float* __restrict__ O,
                                                      int ldo, int causal) {
     if (!plan_ok(pa, score_cap)) return;
-    __shared__ float Ps[kTile][kTile + 1], Vs[kTile][kHeadDim + 1];
+    __shared__ float Ps[kTile][kF32Row], Vs[kTile][kHeadDim + 32];
     const int n_items = pa.status[2];
     const int H = pa.heads;
-    const int tx = threadIdx.x % 16, ty = threadIdx.x / 16;
+    const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
+    const int l32 = lane % 32, h2 = lane / 32;
+    const int wq = wave >> 1, wc = wave & 1;
     for (int it = blockIdx.x; it < n_items; it += gridDim.x) {
         const int b = pa.av_items[3 * it], h = pa.av_items[3 * it + 1], ti = pa.av_items[3 * it + 2];
         const int L = pa.lengths[b];
         const int t0 = pa.tok_off[b];
         const int64_t base = pa.att_off[b];
         const int rows = min(kTile, L - ti * kTile);
-        float acc[4][4] = {};
+        floatx16 acc;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc[r] = 0.f;
         const int jend = causal ? min(L, (ti + 1) * kTile) : L;
         for (int j0 = 0; j0 < jend; j0 += kTile) {
             const int cols = min(kTile, L - j0);
@@ -642,26 +653,16 @@ __global__ __launch_bounds__(256) void k_attn_v_f32(PlanArgs pa, const float* __
                 Vs[r][c] = r < cols ? v[(int64_t)(t0 + j0 + r) * ldv + h * kHeadDim + c] : 0.f;
             }
             __syncthreads();
-            for (int j = 0; j < kTile; ++j) {
-                float a[4], bb[4];
-#pragma unroll
-                for (int u = 0; u < 4; ++u) {
-                    a[u] = Ps[ty * 4 + u][j];
-                    bb[u] = Vs[j][tx + 16 * u];
-                }
-#pragma unroll
-                for (int u = 0; u < 4; ++u)
-#pragma unroll
-                    for (int w = 0; w < 4; ++w) acc[u][w] = fmaf(a[u], bb[w], acc[u][w]);
-            }
+#pragma unroll 8
+            for (int kk = 0; kk < kTile; kk += 2)
+                acc = __builtin_amdgcn_mfma_f32_32x32x2f32(Ps[wq * 32 + l32][kk + h2], Vs[kk + h2][wc * 32 + l32], acc,
+                                                           0, 0, 0);
         }
+        float* orow = O + (int64_t)(t0 + ti * kTile) * ldo + h * kHeadDim + wc * 32 + l32;
 #pragma unroll
-        for (int u = 0; u < 4; ++u) {
-            const int i = ty * 4 + u;
-            if (i >= rows) continue;
-#pragma unroll
-            for (int w = 0; w < 4; ++w)
-                O[(int64_t)(t0 + ti * kTile + i) * ldo + h * kHeadDim + tx + 16 * w] = acc[u][w];
+        for (int r = 0; r < 16; ++r) {
+            const int i = wq * 32 + 8 * (r / 4) + 4 * h2 + r % 4;
+            if (i < rows) orow[(int64_t)i * ldo] = acc[r];
         }
     }
 }
