@@ -226,3 +226,52 @@ def test_layer_building_its_plan_reports_data_errors():
     rag.encoder_layer(plan, x, y, wd, dff, ws, flags=flags)
     torch.cuda.synchronize()
     assert plan.data_errors() and "token" in " ".join(plan.data_errors()).lower(), plan.data_errors()
+
+
+@pytest.mark.parametrize("T,H,dff,causal", [(35475, 16, 4096, False), (10076, 8, 2048, True), (1001, 2, 256, False),
+                                            (777, 32, 512, False), (300, 33, 256, False)])
+def test_layer_equals_operator_chain(T, H, dff, causal):
+    # encoder_layer against the same nine operators called one by one through the
+    # operator interface, bit for bit, at the batch-128 d1024 shape, the skewed
+    # batch (masked) and small odd shapes (d from 128 to 2112, T not a multiple
+    # of the tile heights)
+    import paper_2110_10221_amd as rag
+
+    d = H * 64
+    rng = np.random.default_rng(T)
+    L = rng.integers(1, 600, size=T)
+    L = L[np.cumsum(L) < T]
+    L = np.append(L, T - L.sum()).astype(np.int32)  # lengths in [1, 600) summing to T
+    print(f"layer vs operator chain: T={T} B={len(L)} d={d} d_ff={dff} causal={causal}", flush=True)
+    g = torch.Generator(device="cuda").manual_seed(T)
+    rnd = lambda *shape, s=1.0: (torch.randn(*shape, device="cuda", generator=g) * s).bfloat16()
+    x = rnd(T, d)
+    w = {"w_qkv": rnd(3 * d, d, s=0.03), "w_o": rnd(d, d, s=0.03), "w_ff1": rnd(dff, d, s=0.03),
+         "w_ff2": rnd(d, dff, s=0.03), "b_qkv": rnd(3 * d, s=0.1), "b_o": rnd(d, s=0.1), "b_ff1": rnd(dff, s=0.1),
+         "b_ff2": rnd(d, s=0.1), "ln1_g": 1 + rnd(d, s=0.1), "ln1_b": rnd(d, s=0.1), "ln2_g": 1 + rnd(d, s=0.1),
+         "ln2_b": rnd(d, s=0.1)}
+    lens = torch.from_numpy(L).cuda()
+    plan = rag.Plan(lens, T, int(L.max()), H)
+    rag.ragged_offsets(plan)
+    flags = rag.RAG_LAYER_CAUSAL if causal else 0
+    ws = torch.empty(rag.encoder_layer_workspace(T, int(L.max()), d, H, dff, rag.RAG_BF16, flags), dtype=torch.uint8,
+                     device="cuda")
+    y = torch.empty(T, d, dtype=torch.bfloat16, device="cuda")
+    rag.encoder_layer(plan, x, y, w, dff, ws, flags=flags)
+    qkv = torch.empty(T, 3 * d, dtype=torch.bfloat16, device="cuda")
+    rag.packed_linear(x, w["w_qkv"], qkv, bias=w["b_qkv"])
+    o = torch.empty(T, d, dtype=torch.bfloat16, device="cuda")
+    attn = rag.ragged_attention_causal if causal else rag.ragged_attention
+    attn(plan, qkv[:, :d], qkv[:, d:2 * d], qkv[:, 2 * d:], o, 0.125)
+    y1, h1, y2, out = (torch.empty(T, d, dtype=torch.bfloat16, device="cuda") for _ in range(4))
+    rag.packed_linear(o, w["w_o"], y1, bias=w["b_o"], residual=x)
+    rag.packed_layernorm(y1, w["ln1_g"], w["ln1_b"], h1)
+    f = torch.empty(T, dff, dtype=torch.bfloat16, device="cuda")
+    rag.packed_linear(h1, w["w_ff1"], f, bias=w["b_ff1"], act=rag.RAG_ACT_GELU_ERF)
+    rag.packed_linear(f, w["w_ff2"], y2, bias=w["b_ff2"], residual=h1)
+    rag.packed_layernorm(y2, w["ln2_g"], w["ln2_b"], out)
+    torch.cuda.synchronize()
+    assert not plan.data_errors()
+    assert torch.isfinite(out.float()).all()
+    diff = (y.view(torch.int16) != out.view(torch.int16)).sum().item()
+    assert diff == 0, f"{diff} of {T * d} outputs differ"
