@@ -198,30 +198,43 @@ __device__ __forceinline__ void wait_copies(int n) {
 // reduction the tile runs.
 //   W_KN  w is instead [K rows][N] with leading dimension ldw and kvalid valid
 //         rows (rows past it read as zeros): y = x w.
+//   GROUPS = 2  the workgroup has eight waves in two groups of four; group g
+//         runs the K loop over k in [g K / 2, (g + 1) K / 2) in LDS of its own
+//         (smem holds twice tile_lds_bytes), and the epilogue adds the two
+//         groups' fp32 tiles (group 0's first) before bias, activation and
+//         residual: twice the waves on a tile, for launches with fewer tiles
+//         than CUs.  K / 2 is then a multiple of 64.
 //   TRI   x is lower triangular: x[i][k] counts only for k <= i.  The K steps
 //         wholly below the tile's first row run unchecked; the others zero the
 //         fragment entries with k > i after reading them (operation splitting of
 //         the reduction loop's last iterations, Section 4).
-template <int BM, int ACT, bool HAS_BIAS, bool HAS_RES, bool W_KN = false, bool TRI = false>
+template <int BM, int ACT, bool HAS_BIAS, bool HAS_RES, bool W_KN = false, bool TRI = false, int GROUPS = 1>
 __device__ __forceinline__ void gemm_tile_bf16(const uint16_t* __restrict__ x, int ldx, const uint16_t* __restrict__ w,
                                                const uint16_t* __restrict__ bias, const uint16_t* residual, int ldr,
                                                uint16_t* y, int ldy, int T, int K, int N, int m0, int n0,
                                                uint16_t* smem, int ldw = 0, int kvalid = 0) {
     using C = Cfg<BM>;
+    static_assert(GROUPS == 1 || (GROUPS == 2 && !W_KN && !TRI), "K halves: the plain GEMM only");
     constexpr int kStages = C::kStages, kStageElems = C::kStageElems, kCopies = C::kCopies;
     constexpr bool kPW = pair_w(W_KN, TRI);
     constexpr int FM = C::kFM;
     // wave-uniform by construction; made explicit so that LDS copy addresses stay scalar
-    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave), lane = threadIdx.x % kWave;
+    const int wave_all = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave), lane = threadIdx.x % kWave;
+    const int grp = wave_all / C::kWaves;  // the K half (GROUPS = 2)
+    const int wave = wave_all % C::kWaves;
     const int wn = wave;  // the wave's 64 output features
     const int l32 = lane % 32, h2 = lane / 32;
+    uint16_t* const smem_all = smem;
+    if constexpr (GROUPS > 1) smem += grp * (tile_lds_bytes<BM, W_KN, TRI>() / 2);
+    const int kofs = grp * (K / GROUPS);  // the group's first k
 
-    const __amdgpu_buffer_rsrc_t rx = make_rsrc(x + (int64_t)m0 * ldx, (uint32_t)min(T - m0, BM) * ldx * 2u);
+    const __amdgpu_buffer_rsrc_t rx =
+        make_rsrc(x + (int64_t)m0 * ldx + kofs, (uint32_t)min(T - m0, BM) * ldx * 2u);
     __amdgpu_buffer_rsrc_t rw;
     if constexpr (W_KN)  // through the last valid column of the last valid row
         rw = make_rsrc(w + n0, kvalid > 0 ? (uint32_t)(((int64_t)(kvalid - 1) * ldw + min(N - n0, BN)) * 2) : 0u);
     else
-        rw = make_rsrc(w + (int64_t)n0 * K, (uint32_t)min(N - n0, BN) * K * 2u);
+        rw = make_rsrc(w + (int64_t)n0 * K + kofs, (uint32_t)min(N - n0, BN) * K * 2u);
     int vx[C::kXBlocks], vw[C::kWBlocks];
 #pragma unroll
     for (int i = 0; i < C::kXBlocks; ++i) vx[i] = copy_voffset(lane, (wave * C::kXBlocks + i) * kRowsPerBlock, ldx * 2);
@@ -339,7 +352,7 @@ __device__ __forceinline__ void gemm_tile_bf16(const uint16_t* __restrict__ x, i
                 for (int j = 0; j < FM; ++j) acc[i][j] = mfma32x32x16(fa[ks][i], fb[ks][j], acc[i][j]);
     };
 
-    const int nk = K / BK;
+    const int nk = K / GROUPS / BK;
     constexpr std::bool_constant<false> plain{};
     constexpr std::bool_constant<TRI> edge{};
     if constexpr (kPW) {
@@ -468,7 +481,7 @@ __device__ __forceinline__ void gemm_tile_bf16(const uint16_t* __restrict__ x, i
     step_last(fa1, fb1);
     }
 
-    if constexpr (!HAS_RES && !W_KN && !TRI) {
+    if constexpr (!HAS_RES && !W_KN && !TRI && GROUPS == 1) {
         // no residual: bias and activation on the accumulators, bf16 rows staged in
         // LDS all at once (BM rows of 512 bytes, 16-byte chunk c of row r at
         // physical chunk c ^ (r & 31)), then whole rows stored
@@ -520,7 +533,9 @@ __device__ __forceinline__ void gemm_tile_bf16(const uint16_t* __restrict__ x, i
     // store 512-byte rows.  acc[i][j][4g + r] holds (token j*32 + l32, feature
     // i*32 + 8g + 4*h2 + r) of the wave's sub-tile.  LDS layout: row r of 64
     // 16-byte chunks, chunk c at physical slot c ^ r.
-    float* ep = reinterpret_cast<float*>(smem);
+    // (GROUPS = 2: one 32-token slice region per group, the row phase adds them)
+    float* ep = reinterpret_cast<float*>(smem_all);
+    float* const ep_mine = ep + grp * kEpiRows * BN;
     const int ncol = n0 + 4 * lane;  // this lane's four output features in the row phase
     float bv[4] = {0.f, 0.f, 0.f, 0.f};
     if constexpr (HAS_BIAS) {
@@ -532,7 +547,7 @@ __device__ __forceinline__ void gemm_tile_bf16(const uint16_t* __restrict__ x, i
             bv[3] = hi_bf16(bb[1]);
         }
     }
-    constexpr int kRowsPerWave = kEpiRows / C::kWaves;
+    constexpr int kRowsPerWave = kEpiRows / (C::kWaves * GROUPS);
     // Residual rows are fetched for every slice at once, so their latency is paid once per tile.
     u32x2 res[HAS_RES ? BM / kEpiRows : 1][kRowsPerWave];
     if constexpr (HAS_RES) {
@@ -540,7 +555,7 @@ __device__ __forceinline__ void gemm_tile_bf16(const uint16_t* __restrict__ x, i
         for (int slice = 0; slice < BM / kEpiRows; ++slice)
 #pragma unroll
             for (int rr = 0; rr < kRowsPerWave; ++rr) {
-                const int m = m0 + slice * kEpiRows + wave * kRowsPerWave + rr;
+                const int m = m0 + slice * kEpiRows + wave_all * kRowsPerWave + rr;
                 res[slice][rr] = (m < T && ncol < N) ? *reinterpret_cast<const u32x2*>(residual + (int64_t)m * ldr + ncol)
                                                      : u32x2{0u, 0u};
             }
@@ -556,15 +571,20 @@ __device__ __forceinline__ void gemm_tile_bf16(const uint16_t* __restrict__ x, i
                 const int c = (wn * WN + i * 32 + 8 * g + 4 * h2) >> 2;
                 const floatx16& a = acc[i][slice];
                 const floatx4 o = {a[4 * g], a[4 * g + 1], a[4 * g + 2], a[4 * g + 3]};
-                *reinterpret_cast<floatx4*>(ep + (l32 * 64 + (c ^ l32)) * 4) = o;
+                *reinterpret_cast<floatx4*>(ep_mine + (l32 * 64 + (c ^ l32)) * 4) = o;
             }
         barrier_lds();
 #pragma unroll
         for (int rr = 0; rr < kRowsPerWave; ++rr) {
-            const int r = wave * kRowsPerWave + rr;
+            const int r = wave_all * kRowsPerWave + rr;
             const int m = m0 + slice * kEpiRows + r;
             if (m < T && ncol < N) {
-                const floatx4 o = *reinterpret_cast<const floatx4*>(ep + (r * 64 + (lane ^ r)) * 4);
+                floatx4 o = *reinterpret_cast<const floatx4*>(ep + (r * 64 + (lane ^ r)) * 4);
+                if constexpr (GROUPS == 2) {
+                    const floatx4 o1 = *reinterpret_cast<const floatx4*>(ep + kEpiRows * BN + (r * 64 + (lane ^ r)) * 4);
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) o[e] += o1[e];
+                }
                 float v[4];
 #pragma unroll
                 for (int e = 0; e < 4; ++e) v[e] = activate_bf16<ACT>(o[e] + bv[e]);
@@ -590,7 +610,8 @@ __device__ __forceinline__ void gemm_tile_bf16(const uint16_t* __restrict__ x, i
 // QKV projection carries the prelude that way, in the slots its last round of
 // tiles leaves free.
 static_assert(sizeof(PlanSmem) <= tile_lds_bytes<64, false>(), "the plan's LDS fits the GEMM's");
-static_assert(Cfg<128>::kThreads == kFusedBatch, "the plan body runs one thread per sequence of a full batch");
+static_assert(Cfg<128>::kThreads == kFusedBatch && 2 * Cfg<64>::kThreads == kFusedMaxThreads,
+              "the plan body's workgroup sizes");
 
 template <int ACT, bool HAS_BIAS, bool HAS_RES>
 __global__ __launch_bounds__(Cfg<128>::kThreads) __attribute__((amdgpu_waves_per_eu(2, 2)))
@@ -615,6 +636,30 @@ void k_gemm_bf16(const uint16_t* __restrict__ x, int ldx, const uint16_t* __rest
         gemm_tile_bf16<64, ACT, HAS_BIAS, HAS_RES>(x, ldx, w, bias, residual, ldr, y, ldy, T, K, N, m0, tn * BN,
                                                    smem);
     }
+}
+
+// Launches with at most one 64-token tile per CU (small batches): one tile per
+// workgroup of eight waves, the two groups of four splitting K (GROUPS = 2), so
+// each SIMD holds two waves of the tile instead of one.  Workgroups from n_gemm
+// on build a batch's plan (all eight waves; threads past the batch only help).
+constexpr int kDualLds = 2 * tile_lds_bytes<64, false>();
+static_assert(kDualLds <= 160 * 1024, "LDS budget");
+static_assert(sizeof(PlanSmem) <= kDualLds, "the plan's LDS fits the GEMM's");
+
+template <int ACT, bool HAS_BIAS, bool HAS_RES>
+__global__ __launch_bounds__(2 * Cfg<64>::kThreads)
+void k_gemm_bf16_dual(const uint16_t* __restrict__ x, int ldx, const uint16_t* __restrict__ w,
+                      const uint16_t* __restrict__ bias, const uint16_t* residual, int ldr, uint16_t* y, int ldy,
+                      int T, int K, int N, int tiles_m, int tiles_n, int n_gemm, PlanFillArgs pf) {
+    extern __shared__ __attribute__((aligned(16))) uint16_t smem[];
+    if ((int)blockIdx.x >= n_gemm) {
+        plan_fused_body(pf, blockIdx.x - n_gemm, *reinterpret_cast<PlanSmem*>(smem));
+        return;
+    }
+    int tm, tn;
+    tile_coords(blockIdx.x, n_gemm, tiles_m, tiles_n, tm, tn);
+    gemm_tile_bf16<64, ACT, HAS_BIAS, HAS_RES, false, false, 2>(x, ldx, w, bias, residual, ldr, y, ldy, T, K, N,
+                                                                tm * 64, tn * BN, smem);
 }
 
 // fp32: 64x64 tiles, K step 16, 4x4 outputs per thread, plain FMA.
@@ -1010,6 +1055,23 @@ hipError_t launch_bf16_tiles(const void* x, int ldx, const void* w, const void* 
     constexpr int kLds = tile_lds_bytes<128, false>() > tile_lds_bytes<64, false>() ? tile_lds_bytes<128, false>()
                                                                                     : tile_lds_bytes<64, false>();
     const int tiles_m = (T + 127) / 128, tiles_n = (N + BN - 1) / BN, tiles = tiles_m * tiles_n;
+    const int tiles64 = (T + 63) / 64 * tiles_n;
+    const PlanFillArgs pf = plan ? plan_fill_args(*plan) : PlanFillArgs{};
+    if (tiles64 <= device_cu_count() && K % 128 == 0) {  // a small launch: eight waves per tile
+        static bool dual_set = false;  // benign race: every thread sets the same value
+        if (!dual_set) {
+            hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_gemm_bf16_dual<ACT, HB, HR>),
+                                               hipFuncAttributeMaxDynamicSharedMemorySize, kDualLds);
+            if (e != hipSuccess) return e;
+            dual_set = true;
+        }
+        hipLaunchKernelGGL((k_gemm_bf16_dual<ACT, HB, HR>), dim3(tiles64 + (plan ? plan->batch : 0)),
+                           dim3(2 * Cfg<64>::kThreads), kDualLds, s, static_cast<const uint16_t*>(x), ldx,
+                           static_cast<const uint16_t*>(w), static_cast<const uint16_t*>(bias),
+                           static_cast<const uint16_t*>(residual), ldr, static_cast<uint16_t*>(y), ldy, T, K, N,
+                           (T + 63) / 64, tiles_n, tiles64, pf);
+        return hipGetLastError();
+    }
     const int slots = 2 * device_cu_count();                      // resident workgroups
     const int last = tiles - (tiles - 1) / slots * slots;         // tiles in the last round, 1..slots
     const int n_full = 2 * last <= slots ? tiles - last : tiles;  // the rest run as halves
@@ -1021,7 +1083,6 @@ hipError_t launch_bf16_tiles(const void* x, int ldx, const void* w, const void* 
         attr_set = true;
     }
     const int n_gemm = n_full + 2 * (tiles - n_full);
-    const PlanFillArgs pf = plan ? plan_fill_args(*plan) : PlanFillArgs{};
     hipLaunchKernelGGL((k_gemm_bf16<ACT, HB, HR>), dim3(n_gemm + (plan ? plan->batch : 0)), dim3(Cfg<128>::kThreads),
                        kLds, s, static_cast<const uint16_t*>(x), ldx, static_cast<const uint16_t*>(w),
                        static_cast<const uint16_t*>(bias), static_cast<const uint16_t*>(residual), ldr,

@@ -14,7 +14,8 @@
 
 namespace rag {
 
-constexpr int kFusedBatch = 256;  // threads per workgroup, and the largest batch
+constexpr int kFusedBatch = 256;        // the largest batch (one thread per sequence)
+constexpr int kFusedMaxThreads = 512;   // workgroups of kFusedBatch or kFusedMaxThreads threads
 
 struct PlanFillArgs {
     const int32_t* lengths;
@@ -32,7 +33,7 @@ struct PlanFillArgs {
 };
 
 struct PlanSmem {
-    int64_t sh_a[kFusedBatch / kWave], sh_b[kFusedBatch / kWave];
+    int64_t sh_a[kFusedMaxThreads / kWave], sh_b[kFusedMaxThreads / kWave];
     __attribute__((aligned(16))) int32_t sL[kFusedBatch];
     int32_t sOrder[kFusedBatch];
     int flags, max, t0, qoff, aoff;
@@ -86,7 +87,9 @@ inline PlanFillArgs plan_fill_args(const PlanView& p) {
                         p.status};
 }
 
-// Called by all kFusedBatch threads of a workgroup.
+// Called by every thread of a workgroup of kFusedBatch or kFusedMaxThreads
+// threads; thread b < B stands for sequence b, the others only take part in the
+// scans and share the item filling.
 __device__ __forceinline__ void plan_fused_body(const PlanFillArgs& a, int me, PlanSmem& sm) {
     int64_t* const sh_a = sm.sh_a;
     int64_t* const sh_b = sm.sh_b;
@@ -116,7 +119,7 @@ __device__ __forceinline__ void plan_fused_body(const PlanFillArgs& a, int me, P
         sh_max = 0;
     }
     const int L = b < B ? lengths[b] : 0;
-    sL[b] = b < B ? L : -1;  // padding never outranks a length
+    if (b < kFusedBatch) sL[b] = b < B ? L : -1;  // padding never outranks a length
     int flags = 0;
     if (b < B) {
         if (L < 0) flags |= kDataNegLength;
@@ -187,20 +190,20 @@ __device__ __forceinline__ void plan_fused_body(const PlanFillArgs& a, int me, P
     const int nt = (Ls + kTile - 1) / kTile;
     const int nqs = H * nt * nt, nas = H * nt;
     int4* q = reinterpret_cast<int4*>(qkt_items) + sh_qoff;
-    for (int idx = b; idx < nqs; idx += kFusedBatch) {
+    for (int idx = b; idx < nqs; idx += blockDim.x) {
         const int h = idx / (nt * nt), r = idx - h * nt * nt;
         const int ti = r / nt, tj = r - ti * nt;
         q[idx] = make_int4(sb, h, ti, tj);
     }
     int32_t* const av = av_items + 3 * (int64_t)sh_aoff;
-    for (int idx = b; idx < nas; idx += kFusedBatch) {
+    for (int idx = b; idx < nas; idx += blockDim.x) {
         const int h = idx / nt, ti = idx - h * nt;
         av[3 * idx + 0] = sb;
         av[3 * idx + 1] = h;
         av[3 * idx + 2] = ti;
     }
     const int t0 = sh_t0;
-    for (int t = b; t < Ls; t += kFusedBatch) tok_seq[t0 + t] = sb;
+    for (int t = b; t < Ls; t += blockDim.x) tok_seq[t0 + t] = sb;
 }
 
 }  // namespace rag
