@@ -138,7 +138,7 @@ __device__ __forceinline__ u32x4 window16(const u32x4& a, const u32x4& b, int s)
 // any element, so a chunk is cut from two LDS chunks by a funnel shift), and
 // 2-byte stores for the partial chunks at both ends of each row piece.
 constexpr int kPiece = 4 * kTile;         // keys per written row piece: one tile per wave
-constexpr int kPieceRow = kPiece + 8;     // LDS row (elements): room for the shifted read, 4-bank row skew
+constexpr int kPieceRow = kPiece + 4;     // LDS row (elements): room for the shifted read
 __global__ __launch_bounds__(256) void k_qkt_bf16(PlanArgs pa, const uint16_t* __restrict__ q, int ldq,
                                                    const uint16_t* __restrict__ k, int ldk, float scale,
                                                    uint16_t* __restrict__ S, int64_t score_cap, int causal, int G) {
@@ -214,33 +214,38 @@ __global__ __launch_bounds__(256) void k_qkt_bf16(PlanArgs pa, const uint16_t* _
                                   pack_bf16x2(acc[jb][rg][2] * scale, acc[jb][rg][3] * scale)};
             }
             __syncthreads();
-            // Row r holds keys p0 .. p0 + n_r - 1 at elements G_r .. of S.  Pass 1: its
-            // whole 16-byte chunks (row r owns task slots r*M .. r*M + M - 1, M >= the
-            // chunks of any row); pass 2: the partial chunks at both ends of every row.
-            const int M = (pn >> 3) + 1;
-            const int64_t grow = base + ((int64_t)i0 * H + h) * L + p0;  // row 0's first element
-            for (int t = threadIdx.x; t < rows * M; t += 256) {
-                const int r = t / M, cl = t - r * M;
+            // Row r (threads 4 r .. 4 r + 3) holds keys p0 .. p0 + n - 1 at elements G0 ..
+            // G0 + n - 1 of S.  Its whole 16-byte chunks fa .. fb - 1 start at local key
+            // sh + 8 (c - fa), sh = 8 fa - G0 the same for every chunk of the row: five
+            // dwords read from LDS at dword 4 (c - fa) + sh / 2, funneled by 2 (sh & 1)
+            // bytes, give the chunk.  The partial chunks at both ends (under 8 elements
+            // each) are 2-byte stores, two per thread and end.
+            {
+                const int r = threadIdx.x >> 2, sub = threadIdx.x & 3;
                 const int n = causal ? min(pn, i0 + r + 1 - p0) : pn;
-                const int64_t G0 = grow + (int64_t)r * H * L;
-                const int64_t c = ((G0 + 7) >> 3) + cl;
-                if (n > 0 && c < ((G0 + n) >> 3)) {
-                    const int j0 = (int)(8 * c - G0);  // first key (local) of the chunk
-                    const int a0 = j0 & ~7;
-                    const u32x4 lo4 = *reinterpret_cast<const u32x4*>(&st[r][a0]);
-                    const u32x4 hi4 = *reinterpret_cast<const u32x4*>(&st[r][a0 + 8]);
-                    *reinterpret_cast<u32x4*>(S + 8 * c) = window16(lo4, hi4, j0 & 7);
+                if (r < rows && n > 0) {
+                    const int64_t G0 = base + ((int64_t)(i0 + r) * H + h) * L + p0;
+                    const int64_t fa = (G0 + 7) >> 3, fb = (G0 + n) >> 3;
+                    const int sh = (int)(8 * fa - G0);  // 0 .. 7
+                    const int nch = (int)(fb - fa);     // may be negative for a short row
+                    const uint32_t* const src = reinterpret_cast<const uint32_t*>(&st[r][0]) + (sh >> 1);
+                    const uint32_t rb = (sh & 1) * 2;
+                    uint16_t* const dst = S + 8 * fa;
+                    for (int cc = sub; cc < nch; cc += 4) {
+                        const uint32_t* d = src + 4 * cc;
+                        const uint32_t d0 = d[0], d1 = d[1], d2 = d[2], d3 = d[3], d4 = d[4];
+                        *reinterpret_cast<u32x4*>(dst + 8 * cc) =
+                            u32x4{__builtin_amdgcn_alignbyte(d1, d0, rb), __builtin_amdgcn_alignbyte(d2, d1, rb),
+                                  __builtin_amdgcn_alignbyte(d3, d2, rb), __builtin_amdgcn_alignbyte(d4, d3, rb)};
+                    }
+                    const int head = min(sh, n), tail0 = max((int)(8 * fb - G0), head);
+#pragma unroll
+                    for (int u = 0; u < 2; ++u) {
+                        const int eh = sub + 4 * u, et = tail0 + sub + 4 * u;
+                        if (eh < head) S[G0 + eh] = st[r][eh];
+                        if (et < n) S[G0 + et] = st[r][et];
+                    }
                 }
-            }
-            if (threadIdx.x < 2 * rows) {
-                const int r = threadIdx.x >> 1, tail = threadIdx.x & 1;
-                const int n = causal ? min(pn, i0 + r + 1 - p0) : pn;
-                const int64_t G0 = grow + (int64_t)r * H * L;
-                const int64_t fa = (G0 + 7) >> 3, fb = (G0 + n) >> 3;
-                const int head = (int)max<int64_t>(min<int64_t>(8 * fa - G0, n), 0);
-                const int e0 = tail ? (int)max<int64_t>(8 * fb - G0, head) : 0;
-                const int e1 = tail ? max(n, 0) : head;
-                for (int e = e0; e < e1; ++e) S[G0 + e] = st[r][e];
             }
             if (f + 1 < F) {
 #pragma unroll
