@@ -71,7 +71,15 @@ __device__ __forceinline__ int64_t uni64(int64_t v) {
 // QK^T
 // ---------------------------------------------------------------------------
 
-constexpr int kStage = kTile + 8;  // padded LDS row (elements)
+typedef __attribute__((address_space(3))) void lds_void_t;
+
+// Element offset of (row, col) in [rows][64 channels] LDS storage (128-byte rows,
+// two per 256-byte bank line) whose 16-byte chunks are XOR-swizzled by row bits
+// 1-3: the K-operand reads (16 consecutive rows, one chunk each) then meet 16
+// distinct bank groups, and in the transposed V reads (rows r..r+3, four
+// adjacent chunks each) rows r and r+2 use opposite halves of the row.
+__device__ __forceinline__ int kv_swz(int row) { return (((row >> 1) & 1) << 2) | ((row >> 2) & 3); }
+__device__ __forceinline__ int kv_off(int row, int col) { return row * kHeadDim + ((((col >> 3) ^ kv_swz(row)) & 7) << 3) + (col & 7); }
 
 // The bf16 operators take one work item per (sequence, 64-query block, group of
 // G consecutive heads), G a divisor of H chosen at launch so that the batch
@@ -485,18 +493,36 @@ __global__ __launch_bounds__(256) void k_softmax(PlanArgs pa, const typename Ele
 // bf16 Attn.V over the same items as QK^T (one sequence's 64-query block, all
 // heads): the probabilities of the item are one contiguous region; each lane
 // reads its 8 keys of a probability row as two aligned 16-byte chunks
-// (range-checked buffer loads) and a funnel shift.  V tiles are staged
-// transposed in LDS for all four waves.
+// (range-checked buffer loads) and a funnel shift.  V tiles (64 keys x 64
+// channels) reach LDS row-major by bounds-checked direct copies (rows past L_b as
+// zeros) into two buffers, one tile ahead, 16-byte chunks swizzled as in kv_off;
+// the MFMA's V^T operand comes from transposed reads (ds_read_b64_tr_b16: within
+// each 16-lane group, lane 4 e + q addresses row e, columns 4 q .. 4 q + 3 of a
+// 4 x 16 block and lane t receives column t of the four rows), issued as inline
+// assembly with their own wait so that the compiler does not first wait for the
+// next tile's copies.
+constexpr int kAvBuf = kTile * kHeadDim;  // elements of one V buffer
+
 __global__ __launch_bounds__(256) void k_attn_v_bf16(PlanArgs pa, const uint16_t* __restrict__ P,
                                                       int64_t score_cap, const uint16_t* __restrict__ v,
                                                       int ldv, uint16_t* __restrict__ O, int ldo, int causal,
                                                       int G) {
     if (!plan_ok(pa, score_cap)) return;
-    __shared__ __attribute__((aligned(16))) uint16_t Vt[kTile][kStage];  // [c][j]
+    __shared__ __attribute__((aligned(16))) uint16_t vb[2 * kAvBuf];  // [buffer][key][64 channels]
     const int H = pa.heads;
-    const int n_items = pa.status[2] / G, ng = H / G;
-    const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
+    const int n_items = pa.status[2] / G;
+    const int wave = uni(threadIdx.x / kWave), lane = threadIdx.x % kWave;
     const int l16 = lane % 16, q4 = lane / 16;
+    // transposed-read addresses (buffer 0, keys 0..31): group q4 reads keys 8 q4 + e (+ 4),
+    // channels 16 cb + 4 q of its 4 x 16 blocks; keys 32 .. 63 and buffer 1 are immediates
+    // (32 rows leave the swizzle's row bits 1-3 unchanged)
+    const int tr_e = (lane % 16) / 4, tr_q = lane % 4;
+    uint32_t vaddr[4][2];
+#pragma unroll
+    for (int cb = 0; cb < 4; ++cb)
+#pragma unroll
+        for (int hi = 0; hi < 2; ++hi)
+            vaddr[cb][hi] = (uint32_t)(uintptr_t)(vb + kv_off(8 * q4 + tr_e + 4 * hi, 16 * cb + 4 * tr_q));
     for (int base_it = 0; base_it < n_items; base_it += gridDim.x) {
         const int g = base_it + op_item(blockIdx.x, gridDim.x);
         if (g >= n_items) break;  // uniform over the workgroup
@@ -523,62 +549,54 @@ __global__ __launch_bounds__(256) void k_attn_v_bf16(PlanArgs pa, const uint16_t
             __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(P + e_al), 0, (uint32_t)nbytes, 0x00020000);
         const int jend = causal ? min(L, (ti + 1) * kTile) : L;  // masked: keys up to the diagonal tile
         const int kmax = causal ? min(L - 1, i) : L - 1;          // last key this row uses
-        // Tiles (head h0 + f / nt, keys 64 (f % nt) ..) in one stream: the V rows and
-        // probability chunks of tile f + 1 are loaded while tile f is computed.
+        // Tiles (head h0 + f / nt, keys 64 (f % nt) ..) in one stream: tile f + 1's V
+        // copies and probability chunks are issued while tile f is computed.
         const int nt = (jend + kTile - 1) / kTile;
         const int F = G * nt;
-        u32x4 vr[2], vn[2], pr[2][2], pn[2][2];
-        auto load_v = [&](int f, u32x4 (&vv)[2]) {
-            const int h = h0 + f / nt, j0 = (f % nt) * kTile, cols = min(kTile, L - j0);
+        // V tile f into buffer f & 1: wave w copies rows 16 w .. 16 w + 15 (two 1 KB blocks)
+        auto copy_v = [&](int f, auto buf) {
+            const int h = h0 + f / nt, j0 = (f % nt) * kTile;
+            const __amdgpu_buffer_rsrc_t rv = __builtin_amdgcn_make_buffer_rsrc(
+                const_cast<uint16_t*>(v + (int64_t)(t0 + j0) * ldv + h * kHeadDim), 0,
+                (uint32_t)min(kTile, L - j0) * ldv * 2u, 0x00020000);
 #pragma unroll
-            for (int r = 0; r < 2; ++r) {
-                const int id = threadIdx.x + 256 * r;
-                const int jj = id >> 3, cc = (id & 7) * 8;
-                vv[r] = jj < cols ? ld16(v + (int64_t)(t0 + j0 + jj) * ldv + h * kHeadDim + cc) : u32x4{0u, 0u, 0u, 0u};
+            for (int u = 0; u < 2; ++u) {
+                const int blk = 2 * wave + u, row = blk * 8 + lane / 8;
+                const int chunk = (lane % 8) ^ kv_swz(row);
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(rv, (lds_void_t*)(vb + decltype(buf)::value * kAvBuf + blk * 512),
+                                                         16, (row * ldv + chunk * 8) * 2, 0, 0, 0);
             }
         };
         // keys j0 + 32 ks + 8 q4 .. + 7 of this lane's row of head h: two aligned chunks
+        // (always loaded, so every lane issues the same four loads; unused keys are masked)
+        u32x4 pr[2][2], pn[2][2];
         auto load_p = [&](int f, u32x4 (&pp)[2][2]) {
             const int h = h0 + f / nt, j0 = (f % nt) * kTile;
             const int64_t row_e = ((int64_t)(wave * 16 + l16) * H + h) * L;  // row start, relative to e_lo
 #pragma unroll
             for (int ks = 0; ks < 2; ++ks) {
                 const int jk = j0 + 32 * ks + 8 * q4;
-                if (row_ok && jk <= kmax) {
-                    const int a0 = (int)(((e_lo - e_al) + row_e + jk) & ~(int64_t)7);
-                    pp[ks][0] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rp, a0 * 2, 0, 0));
-                    pp[ks][1] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rp, a0 * 2 + 16, 0, 0));
-                } else {
-                    pp[ks][0] = pp[ks][1] = u32x4{0u, 0u, 0u, 0u};
-                }
+                const int a0 = (int)(((e_lo - e_al) + row_e + jk) & ~(int64_t)7);
+                pp[ks][0] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rp, a0 * 2, 0, 0));
+                pp[ks][1] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rp, a0 * 2 + 16, 0, 0));
             }
         };
         // the element shift of every row piece: row starts differ by multiples of L only
         const int64_t row_e0 = (int64_t)(wave * 16 + l16) * H * L;
-        load_v(0, vr);
-        load_p(0, pr);
         floatx4 acc[4];
-        for (int f = 0; f < F; ++f) {
+        auto step = [&](int f, auto buf) {
+            constexpr int BUF = decltype(buf)::value;
             const int h = h0 + f / nt, j0 = (f % nt) * kTile;
             if (f % nt == 0) {
 #pragma unroll
                 for (int cb = 0; cb < 4; ++cb) acc[cb] = floatx4{0.f, 0.f, 0.f, 0.f};
             }
-            __syncthreads();  // the previous tile's V reads are done
-            // values: 64 keys x 64 channels, stored transposed [c][j]
-#pragma unroll
-            for (int r = 0; r < 2; ++r) {
-                const int id = threadIdx.x + 256 * r;
-                const int jj = id >> 3, cc = (id & 7) * 8;
-#pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    Vt[cc + 2 * e][jj] = static_cast<uint16_t>(vr[r][e] & 0xffffu);
-                    Vt[cc + 2 * e + 1][jj] = static_cast<uint16_t>(vr[r][e] >> 16);
-                }
-            }
-            __syncthreads();
+            // this wave's copies of V tile f (tile f's probability loads, issued after
+            // them, may stay in flight), then every wave's; buffer f + 1 was last read in step f - 1
+            asm volatile("s_waitcnt vmcnt(4)" ::: "memory");
+            asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
             if (f + 1 < F) {
-                load_v(f + 1, vn);
+                copy_v(f + 1, std::integral_constant<int, 1 - BUF>{});
                 load_p(f + 1, pn);
             }
             const int sh = (int)((e_lo - e_al + row_e0 + (int64_t)h * L + j0) & 7);
@@ -586,17 +604,35 @@ __global__ __launch_bounds__(256) void k_attn_v_bf16(PlanArgs pa, const uint16_t
             for (int ks = 0; ks < 2; ++ks) {
                 const int jk = j0 + 32 * ks + 8 * q4;
                 u32x4 pw = window16(pr[ks][0], pr[ks][1], sh);
-                // keys past the row's last used key count as zero
+                // keys past the row's last used key (and rows past the block) count as zero
 #pragma unroll
                 for (int e = 0; e < 4; ++e) {
                     const int j = jk + 2 * e;
-                    const uint32_t keep = (j <= kmax ? 0x0000ffffu : 0u) | (j + 1 <= kmax ? 0xffff0000u : 0u);
+                    const uint32_t keep = (row_ok && j <= kmax ? 0x0000ffffu : 0u) |
+                                          (row_ok && j + 1 <= kmax ? 0xffff0000u : 0u);
                     pw[e] &= keep;
                 }
                 const bf16x8 pb = as_bf16x8(pw);
+                u32x2 t[4][2];
+                asm volatile(
+                    "ds_read_b64_tr_b16 %0, %8 offset:%16\n\t"
+                    "ds_read_b64_tr_b16 %1, %9 offset:%16\n\t"
+                    "ds_read_b64_tr_b16 %2, %10 offset:%16\n\t"
+                    "ds_read_b64_tr_b16 %3, %11 offset:%16\n\t"
+                    "ds_read_b64_tr_b16 %4, %12 offset:%16\n\t"
+                    "ds_read_b64_tr_b16 %5, %13 offset:%16\n\t"
+                    "ds_read_b64_tr_b16 %6, %14 offset:%16\n\t"
+                    "ds_read_b64_tr_b16 %7, %15 offset:%16\n\t"
+                    "s_waitcnt lgkmcnt(0)"
+                    : "=&v"(t[0][0]), "=&v"(t[0][1]), "=&v"(t[1][0]), "=&v"(t[1][1]), "=&v"(t[2][0]), "=&v"(t[2][1]),
+                      "=&v"(t[3][0]), "=&v"(t[3][1])
+                    : "v"(vaddr[0][0]), "v"(vaddr[0][1]), "v"(vaddr[1][0]), "v"(vaddr[1][1]), "v"(vaddr[2][0]),
+                      "v"(vaddr[2][1]), "v"(vaddr[3][0]), "v"(vaddr[3][1]),
+                      "i"((BUF * kAvBuf + 32 * ks * kHeadDim) * 2)
+                    : "memory");
 #pragma unroll
                 for (int cb = 0; cb < 4; ++cb) {
-                    const bf16x8 va = as_bf16x8(*reinterpret_cast<const u32x4*>(&Vt[cb * 16 + l16][32 * ks + 8 * q4]));
+                    const bf16x8 va = as_bf16x8(u32x4{t[cb][0][0], t[cb][0][1], t[cb][1][0], t[cb][1][1]});
                     acc[cb] = mfma16x16x32(va, pb, acc[cb]);  // C[c][i] = sum_j V[j][c] P[i][j]
                 }
             }
@@ -611,13 +647,18 @@ __global__ __launch_bounds__(256) void k_attn_v_bf16(PlanArgs pa, const uint16_t
             }
             if (f + 1 < F) {
 #pragma unroll
-                for (int r = 0; r < 2; ++r) vr[r] = vn[r];
-#pragma unroll
                 for (int ks = 0; ks < 2; ++ks) {
                     pr[ks][0] = pn[ks][0];
                     pr[ks][1] = pn[ks][1];
                 }
             }
+        };
+        asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");  // the previous item's reads are done
+        copy_v(0, std::integral_constant<int, 0>{});
+        load_p(0, pr);
+        for (int f = 0; f < F; f += 2) {
+            step(f, std::integral_constant<int, 0>{});
+            if (f + 1 < F) step(f + 1, std::integral_constant<int, 1>{});
         }
     }
 }
@@ -701,8 +742,6 @@ __global__ __launch_bounds__(256) void k_attn_v_f32(PlanArgs pa, const float* __
 // K / V rows in that XCD's L2), the runs round-robin.
 // ---------------------------------------------------------------------------
 
-typedef __attribute__((address_space(3))) void lds_void_t;
-
 constexpr float kRescaleSlack = 8.f;  // log2 of the largest exponential kept
 constexpr int kStreamWaves = 2, kStreamThreads = kStreamWaves * kWave;
 constexpr int kStreamBlocks = 4 / kStreamWaves;                 // 1 KB copies of K (and of V) per wave and chunk
@@ -715,14 +754,6 @@ __device__ __forceinline__ int stream_item(int bid, int nb) {  // nb: a multiple
     const int xcd = bid % 8, j = bid / 8;
     return ((j / kStreamRun) * 8 + xcd) * kStreamRun + j % kStreamRun;
 }
-
-// Element offset of (row, col) in [rows][64 channels] LDS storage (128-byte rows,
-// two per 256-byte bank line) whose 16-byte chunks are XOR-swizzled by row bits
-// 1-3: the K-operand reads (16 consecutive rows, one chunk each) then meet 16
-// distinct bank groups, and in the transposed V reads (rows r..r+3, four
-// adjacent chunks each) rows r and r+2 use opposite halves of the row.
-__device__ __forceinline__ int kv_swz(int row) { return (((row >> 1) & 1) << 2) | ((row >> 2) & 3); }
-__device__ __forceinline__ int kv_off(int row, int col) { return row * kHeadDim + ((((col >> 3) ^ kv_swz(row)) & 7) << 3) + (col & 7); }
 
 __device__ __forceinline__ void attn_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
 
