@@ -491,9 +491,12 @@ __global__ __launch_bounds__(256) void k_softmax(PlanArgs pa, const typename Ele
 // ---------------------------------------------------------------------------
 
 // bf16 Attn.V over the same items as QK^T (one sequence's 64-query block, all
-// heads): the probabilities of the item are one contiguous region; each lane
-// reads its 8 keys of a probability row as two aligned 16-byte chunks
-// (range-checked buffer loads) and a funnel shift.  V tiles (64 keys x 64
+// heads): the probabilities of the item are one contiguous region.  Per tile of
+// 64 keys, each of the block's 64 probability rows is copied to LDS as the ten
+// aligned 16-byte chunks from the one holding its first key on (range-checked
+// direct copies; chunks past the item read as zeros and are masked), and a lane
+// takes its 8 keys as five dwords at the row's element shift, funneled by one
+// byte-align per dword.  V tiles (64 keys x 64
 // channels) reach LDS row-major by bounds-checked direct copies (rows past L_b as
 // zeros) into two buffers, one tile ahead, 16-byte chunks swizzled as in kv_off;
 // the MFMA's V^T operand comes from transposed reads (ds_read_b64_tr_b16: within
@@ -502,6 +505,9 @@ __global__ __launch_bounds__(256) void k_softmax(PlanArgs pa, const typename Ele
 // assembly with their own wait so that the compiler does not first wait for the
 // next tile's copies.
 constexpr int kAvBuf = kTile * kHeadDim;  // elements of one V buffer
+constexpr int kAvPRow = 10;               // 16-byte chunks staged per probability row
+constexpr int kAvPBlocks = 12;            // 1 KB copy blocks per tile: 64 rows x 10 chunks, rounded to 3 per wave
+constexpr int kAvPBuf = kAvPBlocks * 512; // elements of one probability buffer
 
 __global__ __launch_bounds__(256) void k_attn_v_bf16(PlanArgs pa, const uint16_t* __restrict__ P,
                                                       int64_t score_cap, const uint16_t* __restrict__ v,
@@ -509,6 +515,7 @@ __global__ __launch_bounds__(256) void k_attn_v_bf16(PlanArgs pa, const uint16_t
                                                       int G) {
     if (!plan_ok(pa, score_cap)) return;
     __shared__ __attribute__((aligned(16))) uint16_t vb[2 * kAvBuf];  // [buffer][key][64 channels]
+    __shared__ __attribute__((aligned(16))) uint16_t pb[2 * kAvPBuf];  // [buffer][row][10 chunks]
     const int H = pa.heads;
     const int n_items = pa.status[2] / G;
     const int wave = uni(threadIdx.x / kWave), lane = threadIdx.x % kWave;
@@ -567,18 +574,18 @@ __global__ __launch_bounds__(256) void k_attn_v_bf16(PlanArgs pa, const uint16_t
                                                          16, (row * ldv + chunk * 8) * 2, 0, 0, 0);
             }
         };
-        // keys j0 + 32 ks + 8 q4 .. + 7 of this lane's row of head h: two aligned chunks
-        // (always loaded, so every lane issues the same four loads; unused keys are masked)
-        u32x4 pr[2][2], pn[2][2];
-        auto load_p = [&](int f, u32x4 (&pp)[2][2]) {
+        // probability rows of tile f into buffer f & 1: slot x = 64 blk + lane is row x / 10,
+        // chunk x % 10 (slots past 640 copy nothing useful), wave w taking blocks w, w + 4, w + 8
+        auto copy_p = [&](int f, auto buf) {
             const int h = h0 + f / nt, j0 = (f % nt) * kTile;
-            const int64_t row_e = ((int64_t)(wave * 16 + l16) * H + h) * L;  // row start, relative to e_lo
 #pragma unroll
-            for (int ks = 0; ks < 2; ++ks) {
-                const int jk = j0 + 32 * ks + 8 * q4;
-                const int a0 = (int)(((e_lo - e_al) + row_e + jk) & ~(int64_t)7);
-                pp[ks][0] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rp, a0 * 2, 0, 0));
-                pp[ks][1] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rp, a0 * 2 + 16, 0, 0));
+            for (int u = 0; u < kAvPBlocks / 4; ++u) {
+                const int blk = wave + 4 * u, x = blk * 64 + lane;
+                const int r = min(x / kAvPRow, kTile - 1), c = x - (x / kAvPRow) * kAvPRow;
+                const int64_t e = (e_lo - e_al) + ((int64_t)r * H + h) * L + j0;  // the row's first key
+                const int off = x < kTile * kAvPRow ? (int)((e & ~(int64_t)7) + 8 * c) * 2 : 0x7ffffff0;
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(rp, (lds_void_t*)(pb + decltype(buf)::value * kAvPBuf + blk * 512),
+                                                         16, off, 0, 0, 0);
             }
         };
         // the element shift of every row piece: row starts differ by multiples of L only
@@ -591,19 +598,24 @@ __global__ __launch_bounds__(256) void k_attn_v_bf16(PlanArgs pa, const uint16_t
 #pragma unroll
                 for (int cb = 0; cb < 4; ++cb) acc[cb] = floatx4{0.f, 0.f, 0.f, 0.f};
             }
-            // this wave's copies of V tile f (tile f's probability loads, issued after
-            // them, may stay in flight), then every wave's; buffer f + 1 was last read in step f - 1
-            asm volatile("s_waitcnt vmcnt(4)" ::: "memory");
+            // this wave's copies of tile f, then every wave's; buffers f + 1 were last read in step f - 1
+            asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
             asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
             if (f + 1 < F) {
                 copy_v(f + 1, std::integral_constant<int, 1 - BUF>{});
-                load_p(f + 1, pn);
+                copy_p(f + 1, std::integral_constant<int, 1 - BUF>{});
             }
             const int sh = (int)((e_lo - e_al + row_e0 + (int64_t)h * L + j0) & 7);
+            const uint32_t rb = (sh & 1) * 2;
+            const uint32_t* const prow =
+                reinterpret_cast<const uint32_t*>(pb + BUF * kAvPBuf) + (wave * 16 + l16) * (kAvPRow * 4) + (sh >> 1);
 #pragma unroll
             for (int ks = 0; ks < 2; ++ks) {
                 const int jk = j0 + 32 * ks + 8 * q4;
-                u32x4 pw = window16(pr[ks][0], pr[ks][1], sh);
+                const uint32_t* d = prow + 16 * ks + 4 * q4;
+                const uint32_t d0 = d[0], d1 = d[1], d2 = d[2], d3 = d[3], d4 = d[4];
+                u32x4 pw = {__builtin_amdgcn_alignbyte(d1, d0, rb), __builtin_amdgcn_alignbyte(d2, d1, rb),
+                            __builtin_amdgcn_alignbyte(d3, d2, rb), __builtin_amdgcn_alignbyte(d4, d3, rb)};
                 // keys past the row's last used key (and rows past the block) count as zero
 #pragma unroll
                 for (int e = 0; e < 4; ++e) {
@@ -645,17 +657,10 @@ __global__ __launch_bounds__(256) void k_attn_v_bf16(PlanArgs pa, const uint16_t
                     *reinterpret_cast<u32x2*>(orow + cb * 16 + 4 * q4) = w2;
                 }
             }
-            if (f + 1 < F) {
-#pragma unroll
-                for (int ks = 0; ks < 2; ++ks) {
-                    pr[ks][0] = pn[ks][0];
-                    pr[ks][1] = pn[ks][1];
-                }
-            }
         };
         asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");  // the previous item's reads are done
         copy_v(0, std::integral_constant<int, 0>{});
-        load_p(0, pr);
+        copy_p(0, std::integral_constant<int, 0>{});
         for (int f = 0; f < F; f += 2) {
             step(f, std::integral_constant<int, 0>{});
             if (f + 1 < F) step(f + 1, std::integral_constant<int, 1>{});
