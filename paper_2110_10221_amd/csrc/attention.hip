@@ -730,10 +730,12 @@ __global__ __launch_bounds__(256) void k_attn_v_f32(PlanArgs pa, const float* __
 //          directly, 16-byte chunks XOR-swizzled by row, rows past L_b as zeros
 //   scores S^T = K Q^T with v_mfma_f32_32x32x16_bf16 (lane holds query
 //          i = lane % 32 and keys 8*(r/4) + 4*(lane/32) + r%4), kept in fp32
-//   softmax online: z = s * scale * log2(e); a per-row reference m, raised
-//          only when a chunk's maximum exceeds it by more than 8 (so
-//          exp2(z - m) <= 2^8 and the rescaling of the running sum and output
-//          is rare); e = exp2(z - m) rounded to bf16 is the MFMA operand
+//   softmax online: z = s * scale * log2(e); a per-row reference m, the
+//          first chunk's maximum; a later chunk takes e = exp2(z - m) at once
+//          and only if a lane's sum of its 16 exponentials passes 2^16 does
+//          the wave recompute the chunk, raise m to its maximum and rescale
+//          the running sum and output (rare); e rounded to bf16 is the MFMA
+//          operand
 //   output O^T += V^T E^T.  The lane's eight keys of each 16-key step
 //          {4h..4h+3, 8+4h..8+4h+3} (h = lane/32) are its k values (the MFMA
 //          pairs the k-th element of A with the k-th element of B), and
@@ -747,7 +749,7 @@ __global__ __launch_bounds__(256) void k_attn_v_f32(PlanArgs pa, const float* __
 // K / V rows in that XCD's L2), the runs round-robin.
 // ---------------------------------------------------------------------------
 
-constexpr float kRescaleSlack = 8.f;  // log2 of the largest exponential kept
+constexpr float kSumCap = 65536.f;  // largest lane sum of a chunk's exponentials kept (2^16)
 constexpr int kStreamWaves = 2, kStreamThreads = kStreamWaves * kWave;
 constexpr int kStreamBlocks = 4 / kStreamWaves;                 // 1 KB copies of K (and of V) per wave and chunk
 constexpr int kStreamChunk = 32;                                // keys per LDS stage
@@ -872,64 +874,105 @@ void k_attention_bf16(PlanArgs pa, const uint16_t* __restrict__ q, int ldq, cons
             if (!active || c >= nc_me) return;
             const uint16_t* kst = kvs + STG * kStreamStageElems;
             floatx16 acc;
+            // scores of the chunk (rows past L and, causal, keys past the query as -inf)
+            // (LEAN: one K fragment at a time, for the rare recomputation, where the
+            // transposed V reads are already held)
+            auto scores = [&](auto lean) {
 #pragma unroll
-            for (int r = 0; r < 16; ++r) acc[r] = 0.f;
-            bf16x8 kf[4];
+                for (int r = 0; r < 16; ++r) acc[r] = 0.f;
+                if constexpr (decltype(lean)::value) {
 #pragma unroll
-            for (int ks = 0; ks < 4; ++ks) kf[ks] = as_bf16x8(*reinterpret_cast<const u32x4*>(kst + koff[ks]));
-            __builtin_amdgcn_sched_barrier(0);
+                    for (int ks = 0; ks < 4; ++ks)
+                        acc = mfma32x32x16(as_bf16x8(*reinterpret_cast<const u32x4*>(kst + koff[ks])), qf[ks], acc);
+                } else {
+                    bf16x8 kf[4];
 #pragma unroll
-            for (int ks = 0; ks < 4; ++ks) acc = mfma32x32x16(kf[ks], qf[ks], acc);
-            if (32 * (c + 1) > L || (CAUSAL && c == qb)) {
-                const int kmax = CAUSAL && c == qb ? min(L - 1, qb * 32 + l32) : L - 1;
+                    for (int ks = 0; ks < 4; ++ks) kf[ks] = as_bf16x8(*reinterpret_cast<const u32x4*>(kst + koff[ks]));
+                    __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-                for (int r = 0; r < 16; ++r)
-                    if (32 * c + 8 * (r / 4) + 4 * h2 + (r % 4) > kmax) acc[r] = -INFINITY;
-            }
-            float cmax = acc[0];
+                    for (int ks = 0; ks < 4; ++ks) acc = mfma32x32x16(kf[ks], qf[ks], acc);
+                }
+                if (32 * (c + 1) > L || (CAUSAL && c == qb)) {
+                    const int kmax = CAUSAL && c == qb ? min(L - 1, qb * 32 + l32) : L - 1;
 #pragma unroll
-            for (int r = 1; r < 16; ++r) cmax = fmaxf(cmax, acc[r]);
-            const float cz = max_xor32(cmax) * zs;
-            const bool raise = cz > m + kRescaleSlack;
-            if (__ballot(raise) != 0) {
-                const float mn = raise ? cz : m;
-                const float alpha = raise ? __builtin_amdgcn_exp2f(m - mn) : 1.f;
+                    for (int r = 0; r < 16; ++r)
+                        if (32 * c + 8 * (r / 4) + 4 * h2 + (r % 4) > kmax) acc[r] = -INFINITY;
+                }
+            };
+            // the row's largest z = s * scale * log2(e) in the chunk (both half-waves)
+            auto chunk_max = [&]() {
+                float cmax = acc[0];
+#pragma unroll
+                for (int r = 1; r < 16; ++r) cmax = fmaxf(cmax, acc[r]);
+                return max_xor32(cmax) * zs;
+            };
+            // exponentials exp2(z - m) in place of the scores; the lane's sum of them
+            auto exps = [&]() {
+#pragma unroll
+                for (int r = 0; r < 16; ++r) acc[r] = __builtin_amdgcn_exp2f(fmaf(acc[r], zs, -m));
+                float p[8];
+#pragma unroll
+                for (int r = 0; r < 8; ++r) p[r] = acc[2 * r] + acc[2 * r + 1];
+#pragma unroll
+                for (int r = 0; r < 4; ++r) p[r] += p[r + 4];
+                return (p[0] + p[2]) + (p[1] + p[3]);
+            };
+            scores(std::false_type{});
+            // the V^T operand of both 16-key halves by transposed reads, issued now
+            // and waited for just before the P.V products, so their latency passes
+            // under the exponentials (inline assembly: the builtin makes the
+            // compiler wait first for every LDS copy in flight, chunk c + 1's included)
+            u32x2 tr[2][2][2];
+            asm volatile(
+                "ds_read_b64_tr_b16 %0, %8 offset:%12\n\t"
+                "ds_read_b64_tr_b16 %1, %9 offset:%12\n\t"
+                "ds_read_b64_tr_b16 %2, %10 offset:%12\n\t"
+                "ds_read_b64_tr_b16 %3, %11 offset:%12\n\t"
+                "ds_read_b64_tr_b16 %4, %8 offset:%13\n\t"
+                "ds_read_b64_tr_b16 %5, %9 offset:%13\n\t"
+                "ds_read_b64_tr_b16 %6, %10 offset:%13\n\t"
+                "ds_read_b64_tr_b16 %7, %11 offset:%13"
+                : "=&v"(tr[0][0][0]), "=&v"(tr[0][0][1]), "=&v"(tr[0][1][0]), "=&v"(tr[0][1][1]),
+                  "=&v"(tr[1][0][0]), "=&v"(tr[1][0][1]), "=&v"(tr[1][1][0]), "=&v"(tr[1][1][1])
+                : "v"(vaddr[0][0]), "v"(vaddr[0][1]), "v"(vaddr[1][0]), "v"(vaddr[1][1]),
+                  "i"(STG * kStreamStageElems * 2), "i"((STG * kStreamStageElems + 16 * kHeadDim) * 2)
+                : "memory");
+            if (c == 0) m = chunk_max();  // the reference starts at the first chunk's maximum
+            float ps = exps();
+            // a lane sum above kSumCap (or NaN) means a score well above m: the wave
+            // recomputes its scores, raises m to the chunk maximum and rescales what
+            // it has summed so far (rare after the first chunks)
+            if (c > 0 && __ballot(!(ps <= kSumCap)) != 0) {
+                scores(std::true_type{});
+                const float mn = fmaxf(m, chunk_max());
+                const float alpha = __builtin_amdgcn_exp2f(m - mn);
                 lsum *= alpha;
 #pragma unroll
                 for (int cb = 0; cb < 2; ++cb)
 #pragma unroll
                     for (int r = 0; r < 16; ++r) oacc[cb][r] *= alpha;
                 m = mn;
+                ps = exps();
             }
+            lsum += ps;
+            // the transposed reads have landed (the registers pass through the wait,
+            // so no use of them moves above it)
+            asm volatile("s_waitcnt lgkmcnt(0)"
+                         : "+v"(tr[0][0][0]), "+v"(tr[0][0][1]), "+v"(tr[0][1][0]), "+v"(tr[0][1][1]),
+                           "+v"(tr[1][0][0]), "+v"(tr[1][0][1]), "+v"(tr[1][1][0]), "+v"(tr[1][1][1])
+                         :
+                         : "memory");
 #pragma unroll
             for (int t = 0; t < 2; ++t) {
                 u32x4 pw;
 #pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    const float e0 = __builtin_amdgcn_exp2f(fmaf(acc[8 * t + 2 * e], zs, -m));
-                    const float e1 = __builtin_amdgcn_exp2f(fmaf(acc[8 * t + 2 * e + 1], zs, -m));
-                    lsum += e0 + e1;
-                    pw[e] = pack_bf16x2(e0, e1);
-                }
+                for (int e = 0; e < 4; ++e) pw[e] = pack_bf16x2(acc[8 * t + 2 * e], acc[8 * t + 2 * e + 1]);
                 const bf16x8 pb = as_bf16x8(pw);
-                // V^T operand by transposed reads, as inline assembly with its wait in
-                // the same statement: the builtin makes the compiler first wait for
-                // every LDS copy in flight, chunk c + 1's included
-                u32x2 tr[2][2];
-                asm volatile(
-                    "ds_read_b64_tr_b16 %0, %4 offset:%8\n\t"
-                    "ds_read_b64_tr_b16 %1, %5 offset:%8\n\t"
-                    "ds_read_b64_tr_b16 %2, %6 offset:%8\n\t"
-                    "ds_read_b64_tr_b16 %3, %7 offset:%8\n\t"
-                    "s_waitcnt lgkmcnt(0)"
-                    : "=&v"(tr[0][0]), "=&v"(tr[0][1]), "=&v"(tr[1][0]), "=&v"(tr[1][1])
-                    : "v"(vaddr[0][0]), "v"(vaddr[0][1]), "v"(vaddr[1][0]), "v"(vaddr[1][1]),
-                      "i"((STG * kStreamStageElems + 16 * t * kHeadDim) * 2)
-                    : "memory");
 #pragma unroll
                 for (int cb = 0; cb < 2; ++cb)
-                    oacc[cb] = mfma32x32x16(as_bf16x8(u32x4{tr[cb][0][0], tr[cb][0][1], tr[cb][1][0], tr[cb][1][1]}), pb,
-                                            oacc[cb]);
+                    oacc[cb] = mfma32x32x16(
+                        as_bf16x8(u32x4{tr[t][cb][0][0], tr[t][cb][0][1], tr[t][cb][1][0], tr[t][cb][1][1]}), pb,
+                        oacc[cb]);
             }
         };
         attn_barrier();  // both stages are free: the previous item's reads are done

@@ -13,9 +13,10 @@ written here independently of it.
   error.  It meets the row-scaled bound |g - o| <= 1e-3 + 2e-2 max_row |o|
   with a wide margin, and its mean error is tiny.
 * Fused attention (reading of its rounding): an emulation of the fused
-  kernel's arithmetic (fp32 scores, online softmax with a reference raised
-  only past a slack of 2^8, bf16 unnormalised exponentials as the P.V
-  operand, one division by the fp32 row sum at the end) against exact
+  kernel's arithmetic (fp32 scores, online softmax whose reference is the
+  first chunk's maximum, raised only when a chunk's exponentials sum past
+  2^16, bf16 unnormalised exponentials as the P.V operand, one division by
+  the fp32 row sum at the end) against exact
   attention (the oracle chain in fp32 on the same bf16 inputs) meets
   |g - o| <= 1e-3 + 2e-2 sum_j p_j |v_j| and a mean error of at most 4e-3 of
   the mean magnitude, while the element-wise bound against the bf16 oracle
@@ -96,35 +97,50 @@ def test_independent_fp32_layer_meets_the_row_scaled_bound(cid):
         assert elem_worst > 0, elem_worst
 
 
-def _fused_emulation(L, H, q, k, v, scale, slack=8.0):
-    """The fused kernel's arithmetic, all query rows of a (sequence, head) at once."""
+def _fused_emulation(L, H, q, k, v, scale, cap=65536.0):
+    """The fused kernel's arithmetic: per (sequence, head), blocks of 32 query rows
+    (one wave) walk the keys 32 at a time.  The first chunk sets each row's
+    reference m to its maximum z = s * |scale| * log2(e); later chunks take
+    e = exp2(z - m) and, if any row's sum over either half of the chunk's keys
+    (the 16 keys one lane holds: key k with bit 2 of k equal to the lane half)
+    exceeds `cap`, the whole block raises m to max(m, chunk maximum), rescales
+    its running sums and outputs and recomputes e."""
     T, d = int(np.sum(L)), H * 64
     qf, kf, vf = (bf16_bits_to_f32(a).reshape(T, d).astype(np.float32) for a in (q, k, v))
     out = np.zeros((T, d), np.float32)
     zs = np.float32(abs(scale) * 1.4426950408889634)
     sign = np.float32(-1.0 if scale < 0 else 1.0)
+    half = (np.arange(32) >> 2) & 1
     t0 = 0
     for n in L:
         n = int(n)
         for h in range(H):
-            Q = qf[t0:t0 + n, h * 64:(h + 1) * 64] * sign
             K = kf[t0:t0 + n, h * 64:(h + 1) * 64]
             V = vf[t0:t0 + n, h * 64:(h + 1) * 64]
-            m = np.full(n, -np.inf, np.float32)
-            lsum = np.zeros(n, np.float32)
-            o = np.zeros((n, 64), np.float32)
-            for c in range(0, n, 32):
-                s = (Q @ K[c:c + 32].T).astype(np.float32)  # [rows, keys of the chunk]
-                cz = s.max(1) * zs
-                raise_ = cz > m + np.float32(slack)
-                alpha = np.where(raise_, np.exp2(np.where(raise_, m - cz, 0)).astype(np.float32), 1).astype(np.float32)
-                lsum *= alpha
-                o *= alpha[:, None]
-                m = np.where(raise_, cz, m).astype(np.float32)
-                e = np.exp2(s * zs - m[:, None]).astype(np.float32)
-                lsum += e.sum(1, dtype=np.float32)
-                o += _rd(e) @ V[c:c + 32]
-            out[t0:t0 + n, h * 64:(h + 1) * 64] = o / lsum[:, None]
+            for r0 in range(0, n, 32):
+                Q = qf[t0 + r0:t0 + min(n, r0 + 32), h * 64:(h + 1) * 64] * sign
+                m = np.full(Q.shape[0], -np.inf, np.float32)
+                lsum = np.zeros(Q.shape[0], np.float32)
+                o = np.zeros((Q.shape[0], 64), np.float32)
+                for c in range(0, n, 32):
+                    s = (Q @ K[c:c + 32].T).astype(np.float32)  # [rows, keys of the chunk]
+                    z = s * zs
+                    if c == 0:
+                        m = z.max(1)
+                    e = np.exp2(z - m[:, None]).astype(np.float32)
+                    if c > 0:
+                        hk = half[:s.shape[1]]
+                        ps = np.stack([e[:, hk == 0].sum(1), e[:, hk == 1].sum(1)], 1)
+                        if not (ps <= cap).all():
+                            mn = np.maximum(m, z.max(1))
+                            alpha = np.exp2(m - mn).astype(np.float32)
+                            lsum *= alpha
+                            o *= alpha[:, None]
+                            m = mn
+                            e = np.exp2(z - m[:, None]).astype(np.float32)
+                    lsum += e.sum(1, dtype=np.float32)
+                    o += _rd(e) @ V[c:c + 32]
+                out[t0 + r0:t0 + r0 + Q.shape[0], h * 64:(h + 1) * 64] = o / lsum[:, None]
         t0 += n
     return out
 
