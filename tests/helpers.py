@@ -144,3 +144,24 @@ def canary_buffer(n: int, dtype: str, pad: int = 4096, device="cuda"):
 def canary_intact(whole: torch.Tensor, n: int, pad: int = 4096) -> bool:
     w = whole.float().cpu()
     return bool(torch.isnan(w[:pad]).all() and torch.isnan(w[pad + n:]).all())
+
+
+def rising_keys(lengths, heads: int, step: float, seed: int, scale: float = 0.125):
+    """bf16 bits of q, k, v for attention whose scores rise with every chunk of 32
+    keys of a sequence: q near a fixed direction, k rows shifted along it so that
+    the scaled score of key j is about step * (j // 32) nats plus noise.  Every
+    later chunk then holds exponentials far above a running reference set by the
+    first chunk (2^23 per 16 nats), so an online softmax must raise its reference
+    at every chunk."""
+    from workloads import to_bf16_bits
+
+    rng = np.random.default_rng(seed)
+    T, d = int(np.sum(lengths)), heads * 64
+    q = 1.0 + 0.1 * rng.standard_normal((T, d))
+    k = 0.1 * rng.standard_normal((T, d))
+    t0 = 0
+    for n in np.asarray(lengths, np.int64):
+        k[t0:t0 + n] += (np.arange(n) // 32)[:, None] * (step / (scale * 64.0))
+        t0 += int(n)
+    v = rng.standard_normal((T, d))
+    return tuple(to_bf16_bits(a.astype(np.float32)) for a in (q, k, v))

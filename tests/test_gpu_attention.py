@@ -10,7 +10,7 @@ import torch
 
 import oracle
 from tests.helpers import (BF16_ATOL, BF16_RTOL, bf16_close, canary_buffer, canary_intact, close, dev, host,
-                           scores_close, values)
+                           rising_keys, scores_close, values)
 from workloads import make_workload, random_storage
 
 pytestmark = pytest.mark.gpu
@@ -189,6 +189,18 @@ def test_fused_attention_every_block_count(H):
     T = int(L.sum())
     print(f"fused block counts H={H}", flush=True)
     q, k, v = (random_storage(rng, (T, H * 64), "bf16", 1.0) for _ in range(3))
+    _fused_close(_fused(L, H, q, k, v, 0.125), L, H, q, k, v, 0.125)
+
+
+@pytest.mark.parametrize("step", [16.0, 40.0])
+def test_fused_attention_reference_raised_every_chunk(step):
+    # scores rising by `step` nats per chunk of 32 keys: every later chunk of every
+    # row passes the kernel's exponential-sum cap, so each one recomputes its
+    # scores, raises the row's reference and rescales the running sums
+    L = np.array([700, 512, 33, 64, 95, 1], np.int32)
+    H = 2
+    print(f"fused rising scores step={step}", flush=True)
+    q, k, v = rising_keys(L, H, step, seed=int(step))
     _fused_close(_fused(L, H, q, k, v, 0.125), L, H, q, k, v, 0.125)
 
 

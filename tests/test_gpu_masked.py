@@ -6,7 +6,7 @@ import torch
 
 import oracle
 from tests.helpers import (BF16_ATOL, BF16_RTOL, bf16_row_close, canary_buffer, canary_intact, close, dev, host,
-                           scores_close, values)
+                           rising_keys, scores_close, values)
 from tests.test_gpu_layer import _gpu_layer, _small_weights
 from workloads import BIAS_NAMES, LN_NAMES, WEIGHT_NAMES, make_workload, random_storage
 
@@ -144,6 +144,16 @@ def test_fused_causal_every_block_count(H):
     T = int(L.sum())
     print(f"fused causal block counts H={H}", flush=True)
     q, k, v = (random_storage(rng, (T, H * 64), "bf16", 1.0) for _ in range(3))
+    _fused_causal_close(_fused_causal(L, H, q, k, v, 0.125), L, H, q, k, v, 0.125)
+
+
+def test_fused_causal_reference_raised_every_chunk():
+    # scores rising by 16 nats per chunk of 32 keys: each row raises its reference
+    # at every chunk up to its own (the diagonal chunk masked past the query)
+    L = np.array([700, 512, 33, 64, 95, 1], np.int32)
+    H = 2
+    print("fused causal rising scores", flush=True)
+    q, k, v = rising_keys(L, H, 16.0, seed=3)
     _fused_causal_close(_fused_causal(L, H, q, k, v, 0.125), L, H, q, k, v, 0.125)
 
 

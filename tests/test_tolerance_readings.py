@@ -27,7 +27,8 @@ import pytest
 import torch
 
 import oracle
-from tests.helpers import BF16_ATOL, BF16_RTOL, ELEM_PASS_MIN, ROW_MEAN_TOL, bf16_row_close, bf16_row_stats, values
+from tests.helpers import (BF16_ATOL, BF16_RTOL, ELEM_PASS_MIN, ROW_MEAN_TOL, bf16_row_close, bf16_row_stats, rising_keys,
+                           values)
 from workloads import BIAS_NAMES, LN_NAMES, WEIGHT_NAMES, bf16_bits_to_f32, make_workload, random_storage
 
 
@@ -97,14 +98,14 @@ def test_independent_fp32_layer_meets_the_row_scaled_bound(cid):
         assert elem_worst > 0, elem_worst
 
 
-def _fused_emulation(L, H, q, k, v, scale, cap=65536.0):
+def _fused_emulation(L, H, q, k, v, scale, cap=65536.0, stats=None):
     """The fused kernel's arithmetic: per (sequence, head), blocks of 32 query rows
     (one wave) walk the keys 32 at a time.  The first chunk sets each row's
     reference m to its maximum z = s * |scale| * log2(e); later chunks take
     e = exp2(z - m) and, if any row's sum over either half of the chunk's keys
     (the 16 keys one lane holds: key k with bit 2 of k equal to the lane half)
     exceeds `cap`, the whole block raises m to max(m, chunk maximum), rescales
-    its running sums and outputs and recomputes e."""
+    its running sums and outputs and recomputes e (counted in stats["raises"])."""
     T, d = int(np.sum(L)), H * 64
     qf, kf, vf = (bf16_bits_to_f32(a).reshape(T, d).astype(np.float32) for a in (q, k, v))
     out = np.zeros((T, d), np.float32)
@@ -132,6 +133,8 @@ def _fused_emulation(L, H, q, k, v, scale, cap=65536.0):
                         hk = half[:s.shape[1]]
                         ps = np.stack([e[:, hk == 0].sum(1), e[:, hk == 1].sum(1)], 1)
                         if not (ps <= cap).all():
+                            if stats is not None:
+                                stats["raises"] = stats.get("raises", 0) + 1
                             mn = np.maximum(m, z.max(1))
                             alpha = np.exp2(m - mn).astype(np.float32)
                             lsum *= alpha
@@ -160,6 +163,27 @@ def test_fused_rounding_emulation_meets_the_fused_bound(Ls, H, qscale):
     got = _rd(_fused_emulation(L, H, q, k, v, scale)).astype(np.float64)  # the kernel stores bf16
     q32, k32, v32 = (bf16_bits_to_f32(a).reshape(T, d).astype(np.float32) for a in (q, k, v))
     P = oracle.softmax("f32", L, H, oracle.qkt("f32", L, H, 64, q32, d, k32, d, scale))
+    exact = np.asarray(oracle.attn_v("f32", L, H, 64, P, v32, d), np.float64).reshape(T, d)
+    mag = np.asarray(oracle.attn_v("f32", L, H, 64, P, np.abs(v32), d), np.float64).reshape(T, d)
+    err = np.abs(got - exact)
+    assert (err - (BF16_ATOL + BF16_RTOL * mag)).max() <= 0
+    assert err.mean() <= 4e-3 * mag.mean()
+
+
+def test_fused_emulation_with_raised_references_meets_the_fused_bound():
+    # scores rising by 16 nats per chunk of 32 keys: every later chunk takes the
+    # raise path (recomputed scores, raised reference, rescaled sums), whose extra
+    # rescaling must stay within the same bound
+    L = np.array([700, 512, 33, 64, 95], np.int32)
+    H = 2
+    T, d = int(L.sum()), H * 64
+    q, k, v = rising_keys(L, H, 16.0, seed=7)
+    stats = {}
+    got = _rd(_fused_emulation(L, H, q, k, v, 0.125, stats=stats)).astype(np.float64)
+    blocks = sum(H * ((n + 31) // 32) * ((n + 31) // 32 - 1) for n in L.tolist())
+    assert stats["raises"] == blocks  # every later chunk of every 32-row block
+    q32, k32, v32 = (bf16_bits_to_f32(a).reshape(T, d).astype(np.float32) for a in (q, k, v))
+    P = oracle.softmax("f32", L, H, oracle.qkt("f32", L, H, 64, q32, d, k32, d, 0.125))
     exact = np.asarray(oracle.attn_v("f32", L, H, 64, P, v32, d), np.float64).reshape(T, d)
     mag = np.asarray(oracle.attn_v("f32", L, H, 64, P, np.abs(v32), d), np.float64).reshape(T, d)
     err = np.abs(got - exact)
