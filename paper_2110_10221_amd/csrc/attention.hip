@@ -152,6 +152,7 @@ __global__ __launch_bounds__(256) void k_qkt_bf16(PlanArgs pa, const uint16_t* _
                                                    uint16_t* __restrict__ S, int64_t score_cap, int causal, int G) {
     if (!plan_ok(pa, score_cap)) return;
     __shared__ __attribute__((aligned(16))) uint16_t st[kTile][kPieceRow];
+    __shared__ __attribute__((aligned(16))) uint16_t qs[2][kTile * kHeadDim];  // a head's Q block, two buffers
     const int H = pa.heads;
     const int n_items = pa.status[2] / G, ng = H / G;
     const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
@@ -175,6 +176,22 @@ __global__ __launch_bounds__(256) void k_qkt_bf16(PlanArgs pa, const uint16_t* _
         const int F = G * npc;
         // this wave's key tile of piece f: head h0 + f / npc, keys (f % npc) * kPiece + 64 wave ..
         bf16x8 kc[4][2], kn[4][2], qf[4][2];
+        // the Q block (rows i0 .. i0 + 63, rows past L as zeros) of head h0 + j into
+        // qs[j & 1] by direct copies: wave w fills rows 16 w .. 16 w + 15 (two 1 KB
+        // blocks of 8 rows), 16-byte chunks swizzled as in kv_off
+        auto copy_q = [&](int j) {
+            const __amdgpu_buffer_rsrc_t rq = __builtin_amdgcn_make_buffer_rsrc(
+                const_cast<uint16_t*>(q + (int64_t)(t0 + i0) * ldq + (h0 + j) * kHeadDim), 0,
+                (uint32_t)rows * ldq * 2u, 0x00020000);
+#pragma unroll
+            for (int i = 0; i < 2; ++i) {
+                const int row = (2 * wave + i) * 8 + lane / 8;
+                const int off = row * ldq * 2 + (((lane % 8) ^ kv_swz(row)) * 16);
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(rq, (lds_void_t*)(&qs[j & 1][(2 * wave + i) * 512]), 16, off,
+                                                         0, 0, 0);
+            }
+        };
+        copy_q(0);
         auto load_k = [&](int f, bf16x8 (&kb)[4][2]) {
             const int h = h0 + f / npc, k0 = (f % npc) * kPiece + wave * kTile;
 #pragma unroll
@@ -188,13 +205,17 @@ __global__ __launch_bounds__(256) void k_qkt_bf16(PlanArgs pa, const uint16_t* _
         load_k(0, kc);
         for (int f = 0; f < F; ++f) {
             const int h = h0 + f / npc, p0 = (f % npc) * kPiece;
-            if (f % npc == 0) {  // a new head: its Q fragments, rows rg*16 + l16
+            if (f % npc == 0) {  // a new head: its Q block has landed (all waves' copies)
+                const int j = f / npc;
+                asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+                __syncthreads();
+                if (j + 1 < G) copy_q(j + 1);  // qs[(j + 1) & 1] was last read by head j - 1
+                // its Q fragments, rows rg*16 + l16
+                const uint16_t* qb = qs[j & 1];
 #pragma unroll
                 for (int rg = 0; rg < 4; ++rg) {
-                    const int qi = min(i0 + rg * 16 + l16, L - 1);
-                    const uint16_t* qrow = q + (int64_t)(t0 + qi) * ldq + h * kHeadDim + 8 * q4;
-                    qf[rg][0] = as_bf16x8(ld16(qrow));
-                    qf[rg][1] = as_bf16x8(ld16(qrow + 32));
+                    qf[rg][0] = as_bf16x8(*reinterpret_cast<const u32x4*>(qb + kv_off(rg * 16 + l16, 8 * q4)));
+                    qf[rg][1] = as_bf16x8(*reinterpret_cast<const u32x4*>(qb + kv_off(rg * 16 + l16, 32 + 8 * q4)));
                 }
             }
             if (f + 1 < F) load_k(f + 1, kn);
