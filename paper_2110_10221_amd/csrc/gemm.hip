@@ -528,36 +528,42 @@ __device__ __forceinline__ void gemm_tile_bf16(const uint16_t* __restrict__ x, i
         return;
     }
     // Epilogue through LDS, 32 tokens at a time: the waves holding a slice write
-    // their fp32 accumulators there, then all waves read whole rows back (16 bytes
-    // per lane, 256 features per row), apply bias, activation and residual and
-    // store 512-byte rows.  acc[i][j][4g + r] holds (token j*32 + l32, feature
-    // i*32 + 8g + 4*h2 + r) of the wave's sub-tile.  LDS layout: row r of 64
-    // 16-byte chunks, chunk c at physical slot c ^ r.
+    // their fp32 accumulators there, then all waves read whole rows back (32
+    // bytes per lane, two rows of 256 features per wave instruction), apply bias,
+    // activation and residual and store 512-byte rows as 16-byte chunks.
+    // acc[i][j][4g + r] holds (token j*32 + l32, feature i*32 + 8g + 4*h2 + r) of
+    // the wave's sub-tile.  LDS layout: row r of 64 16-byte chunks, chunk c at
+    // physical slot c ^ r.
     // (GROUPS = 2: one 32-token slice region per group, the row phase adds them)
     float* ep = reinterpret_cast<float*>(smem_all);
     float* const ep_mine = ep + grp * kEpiRows * BN;
-    const int ncol = n0 + 4 * lane;  // this lane's four output features in the row phase
-    float bv[4] = {0.f, 0.f, 0.f, 0.f};
+    const int cl = lane % 32;        // this lane's 16-byte output chunk of a row in the row phase
+    const int ncol = n0 + 8 * cl;    // its eight output features
+    float bv[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
     if constexpr (HAS_BIAS) {
-        if (ncol < N) {
-            const u32x2 bb = *reinterpret_cast<const u32x2*>(bias + ncol);
-            bv[0] = lo_bf16(bb[0]);
-            bv[1] = hi_bf16(bb[0]);
-            bv[2] = lo_bf16(bb[1]);
-            bv[3] = hi_bf16(bb[1]);
+        if (ncol < N) {  // two 8-byte loads: the bias need only be 8-byte aligned
+#pragma unroll
+            for (int hb = 0; hb < 2; ++hb) {
+                const u32x2 bb = *reinterpret_cast<const u32x2*>(bias + ncol + 4 * hb);
+                bv[4 * hb] = lo_bf16(bb[0]);
+                bv[4 * hb + 1] = hi_bf16(bb[0]);
+                bv[4 * hb + 2] = lo_bf16(bb[1]);
+                bv[4 * hb + 3] = hi_bf16(bb[1]);
+            }
         }
     }
     constexpr int kRowsPerWave = kEpiRows / (C::kWaves * GROUPS);
+    constexpr int kRowPairs = kRowsPerWave / 2;  // wave instructions per slice: rows 2 p + h2
     // Residual rows are fetched for every slice at once, so their latency is paid once per tile.
-    u32x2 res[HAS_RES ? BM / kEpiRows : 1][kRowsPerWave];
+    u32x4 res[HAS_RES ? BM / kEpiRows : 1][kRowPairs];
     if constexpr (HAS_RES) {
 #pragma unroll
         for (int slice = 0; slice < BM / kEpiRows; ++slice)
 #pragma unroll
-            for (int rr = 0; rr < kRowsPerWave; ++rr) {
-                const int m = m0 + slice * kEpiRows + wave_all * kRowsPerWave + rr;
-                res[slice][rr] = (m < T && ncol < N) ? *reinterpret_cast<const u32x2*>(residual + (int64_t)m * ldr + ncol)
-                                                     : u32x2{0u, 0u};
+            for (int rp = 0; rp < kRowPairs; ++rp) {
+                const int m = m0 + slice * kEpiRows + wave_all * kRowsPerWave + 2 * rp + h2;
+                res[slice][rp] = (m < T && ncol < N) ? *reinterpret_cast<const u32x4*>(residual + (int64_t)m * ldr + ncol)
+                                                     : u32x4{0u, 0u, 0u, 0u};
             }
     }
 #pragma unroll
@@ -575,28 +581,37 @@ __device__ __forceinline__ void gemm_tile_bf16(const uint16_t* __restrict__ x, i
             }
         barrier_lds();
 #pragma unroll
-        for (int rr = 0; rr < kRowsPerWave; ++rr) {
-            const int r = wave_all * kRowsPerWave + rr;
+        for (int rp = 0; rp < kRowPairs; ++rp) {
+            const int r = wave_all * kRowsPerWave + 2 * rp + h2;
             const int m = m0 + slice * kEpiRows + r;
             if (m < T && ncol < N) {
-                floatx4 o = *reinterpret_cast<const floatx4*>(ep + (r * 64 + (lane ^ r)) * 4);
-                if constexpr (GROUPS == 2) {
-                    const floatx4 o1 = *reinterpret_cast<const floatx4*>(ep + kEpiRows * BN + (r * 64 + (lane ^ r)) * 4);
+                float o[8];
 #pragma unroll
-                    for (int e = 0; e < 4; ++e) o[e] += o1[e];
+                for (int hc = 0; hc < 2; ++hc) {
+                    const int slot = ((2 * cl + hc) ^ r) * 4;
+                    floatx4 t = *reinterpret_cast<const floatx4*>(ep + r * 256 + slot);
+                    if constexpr (GROUPS == 2) {
+                        const floatx4 t1 = *reinterpret_cast<const floatx4*>(ep + kEpiRows * BN + r * 256 + slot);
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) t[e] += t1[e];
+                    }
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) o[4 * hc + e] = t[e];
                 }
-                float v[4];
+                float v[8];
 #pragma unroll
-                for (int e = 0; e < 4; ++e) v[e] = activate_bf16<ACT>(o[e] + bv[e]);
+                for (int e = 0; e < 8; ++e) v[e] = activate_bf16<ACT>(o[e] + bv[e]);
                 if constexpr (HAS_RES) {
-                    const u32x2 rv = res[HAS_RES ? slice : 0][rr];
-                    v[0] += lo_bf16(rv[0]);
-                    v[1] += hi_bf16(rv[0]);
-                    v[2] += lo_bf16(rv[1]);
-                    v[3] += hi_bf16(rv[1]);
+                    const u32x4 rv = res[HAS_RES ? slice : 0][rp];
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        v[2 * e] += lo_bf16(rv[e]);
+                        v[2 * e + 1] += hi_bf16(rv[e]);
+                    }
                 }
-                *reinterpret_cast<u32x2*>(y + (int64_t)m * ldy + ncol) =
-                    u32x2{pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3])};
+                *reinterpret_cast<u32x4*>(y + (int64_t)m * ldy + ncol) =
+                    u32x4{pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]), pack_bf16x2(v[4], v[5]),
+                          pack_bf16x2(v[6], v[7])};
             }
         }
     }
