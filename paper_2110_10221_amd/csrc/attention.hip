@@ -147,7 +147,11 @@ __device__ __forceinline__ u32x4 window16(const u32x4& a, const u32x4& b, int s)
 // 2-byte stores for the partial chunks at both ends of each row piece.
 constexpr int kPiece = 4 * kTile;         // keys per written row piece: one tile per wave
 constexpr int kPieceRow = kPiece + 4;     // LDS row (elements): room for the shifted read
-__global__ __launch_bounds__(256) void k_qkt_bf16(PlanArgs pa, const uint16_t* __restrict__ q, int ldq,
+constexpr int kQkWaves = 8, kQkThreads = kQkWaves * kWave;
+constexpr int kQkKeys = kPiece / kQkWaves;  // keys of a piece per wave
+constexpr int kQkJb = kQkKeys / 16;         // 16-key MFMA blocks per wave
+
+__global__ __launch_bounds__(kQkThreads) void k_qkt_bf16(PlanArgs pa, const uint16_t* __restrict__ q, int ldq,
                                                    const uint16_t* __restrict__ k, int ldk, float scale,
                                                    uint16_t* __restrict__ S, int64_t score_cap, int causal, int G) {
     if (!plan_ok(pa, score_cap)) return;
@@ -174,28 +178,25 @@ __global__ __launch_bounds__(256) void k_qkt_bf16(PlanArgs pa, const uint16_t* _
         const int kend = causal ? min(L, i0 + rows) : L;
         const int npc = (kend + kPiece - 1) / kPiece;  // pieces per head
         const int F = G * npc;
-        // this wave's key tile of piece f: head h0 + f / npc, keys (f % npc) * kPiece + 64 wave ..
-        bf16x8 kc[4][2], kn[4][2], qf[4][2];
+        // this wave's keys of piece f: head h0 + f / npc, keys (f % npc) * kPiece + kQkKeys wave ..
+        bf16x8 kc[kQkJb][2], kn[kQkJb][2], qf[4][2];
         // the Q block (rows i0 .. i0 + 63, rows past L as zeros) of head h0 + j into
-        // qs[j & 1] by direct copies: wave w fills rows 16 w .. 16 w + 15 (two 1 KB
-        // blocks of 8 rows), 16-byte chunks swizzled as in kv_off
+        // qs[j & 1] by direct copies: wave w fills rows 8 w .. 8 w + 7 (one 1 KB
+        // block), 16-byte chunks swizzled as in kv_off
         auto copy_q = [&](int j) {
             const __amdgpu_buffer_rsrc_t rq = __builtin_amdgcn_make_buffer_rsrc(
                 const_cast<uint16_t*>(q + (int64_t)(t0 + i0) * ldq + (h0 + j) * kHeadDim), 0,
                 (uint32_t)rows * ldq * 2u, 0x00020000);
-#pragma unroll
-            for (int i = 0; i < 2; ++i) {
-                const int row = (2 * wave + i) * 8 + lane / 8;
-                const int off = row * ldq * 2 + (((lane % 8) ^ kv_swz(row)) * 16);
-                __builtin_amdgcn_raw_ptr_buffer_load_lds(rq, (lds_void_t*)(&qs[j & 1][(2 * wave + i) * 512]), 16, off,
-                                                         0, 0, 0);
-            }
+            static_assert(kQkWaves * 8 == kTile, "one 8-row block of Q per wave");
+            const int row = wave * 8 + lane / 8;
+            const int off = row * ldq * 2 + (((lane % 8) ^ kv_swz(row)) * 16);
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(rq, (lds_void_t*)(&qs[j & 1][wave * 512]), 16, off, 0, 0, 0);
         };
         copy_q(0);
-        auto load_k = [&](int f, bf16x8 (&kb)[4][2]) {
-            const int h = h0 + f / npc, k0 = (f % npc) * kPiece + wave * kTile;
+        auto load_k = [&](int f, bf16x8 (&kb)[kQkJb][2]) {
+            const int h = h0 + f / npc, k0 = (f % npc) * kPiece + wave * kQkKeys;
 #pragma unroll
-            for (int jb = 0; jb < 4; ++jb) {
+            for (int jb = 0; jb < kQkJb; ++jb) {
                 const int kj = min(k0 + jb * 16 + l16, L - 1);
                 const uint16_t* krow = k + (int64_t)(t0 + kj) * ldk + h * kHeadDim + 8 * q4;
                 kb[jb][0] = as_bf16x8(ld16(krow));
@@ -220,11 +221,11 @@ __global__ __launch_bounds__(256) void k_qkt_bf16(PlanArgs pa, const uint16_t* _
             }
             if (f + 1 < F) load_k(f + 1, kn);
             const int pn = min(kPiece, kend - p0);
-            const bool mine = wave * kTile < pn;  // this wave's tile holds keys of the piece
-            floatx4 acc[4][4];
+            const bool mine = wave * kQkKeys < pn;  // this wave's keys include keys of the piece
+            floatx4 acc[kQkJb][4];
             if (mine) {
 #pragma unroll
-                for (int jb = 0; jb < 4; ++jb)
+                for (int jb = 0; jb < kQkJb; ++jb)
 #pragma unroll
                     for (int rg = 0; rg < 4; ++rg) {
                         acc[jb][rg] = floatx4{0.f, 0.f, 0.f, 0.f};
@@ -235,22 +236,22 @@ __global__ __launch_bounds__(256) void k_qkt_bf16(PlanArgs pa, const uint16_t* _
             __syncthreads();  // the previous piece's LDS rows are written out
             if (mine) {
 #pragma unroll
-                for (int jb = 0; jb < 4; ++jb)
+                for (int jb = 0; jb < kQkJb; ++jb)
 #pragma unroll
                     for (int rg = 0; rg < 4; ++rg)
-                        *reinterpret_cast<u32x2*>(&st[rg * 16 + l16][wave * kTile + jb * 16 + 4 * q4]) =
+                        *reinterpret_cast<u32x2*>(&st[rg * 16 + l16][wave * kQkKeys + jb * 16 + 4 * q4]) =
                             u32x2{pack_bf16x2(acc[jb][rg][0] * scale, acc[jb][rg][1] * scale),
                                   pack_bf16x2(acc[jb][rg][2] * scale, acc[jb][rg][3] * scale)};
             }
             __syncthreads();
-            // Row r (threads 4 r .. 4 r + 3) holds keys p0 .. p0 + n - 1 at elements G0 ..
+            // Row r (threads 8 r .. 8 r + 7) holds keys p0 .. p0 + n - 1 at elements G0 ..
             // G0 + n - 1 of S.  Its whole 16-byte chunks fa .. fb - 1 start at local key
             // sh + 8 (c - fa), sh = 8 fa - G0 the same for every chunk of the row: five
             // dwords read from LDS at dword 4 (c - fa) + sh / 2, funneled by 2 (sh & 1)
             // bytes, give the chunk.  The partial chunks at both ends (under 8 elements
-            // each) are 2-byte stores, two per thread and end.
+            // each) are 2-byte stores, one per thread and end.
             {
-                const int r = threadIdx.x >> 2, sub = threadIdx.x & 3;
+                const int r = threadIdx.x >> 3, sub = threadIdx.x & 7;
                 const int n = causal ? min(pn, i0 + r + 1 - p0) : pn;
                 if (r < rows && n > 0) {
                     const int64_t G0 = base + ((int64_t)(i0 + r) * H + h) * L + p0;
@@ -260,7 +261,7 @@ __global__ __launch_bounds__(256) void k_qkt_bf16(PlanArgs pa, const uint16_t* _
                     const uint32_t* const src = reinterpret_cast<const uint32_t*>(&st[r][0]) + (sh >> 1);
                     const uint32_t rb = (sh & 1) * 2;
                     uint16_t* const dst = S + 8 * fa;
-                    for (int cc = sub; cc < nch; cc += 4) {
+                    for (int cc = sub; cc < nch; cc += 8) {
                         const uint32_t* d = src + 4 * cc;
                         const uint32_t d0 = d[0], d1 = d[1], d2 = d[2], d3 = d[3], d4 = d[4];
                         *reinterpret_cast<u32x4*>(dst + 8 * cc) =
@@ -268,17 +269,13 @@ __global__ __launch_bounds__(256) void k_qkt_bf16(PlanArgs pa, const uint16_t* _
                                   __builtin_amdgcn_alignbyte(d3, d2, rb), __builtin_amdgcn_alignbyte(d4, d3, rb)};
                     }
                     const int head = min(sh, n), tail0 = max((int)(8 * fb - G0), head);
-#pragma unroll
-                    for (int u = 0; u < 2; ++u) {
-                        const int eh = sub + 4 * u, et = tail0 + sub + 4 * u;
-                        if (eh < head) S[G0 + eh] = st[r][eh];
-                        if (et < n) S[G0 + et] = st[r][et];
-                    }
+                    if (sub < head) S[G0 + sub] = st[r][sub];
+                    if (tail0 + sub < n) S[G0 + tail0 + sub] = st[r][tail0 + sub];
                 }
             }
             if (f + 1 < F) {
 #pragma unroll
-                for (int jb = 0; jb < 4; ++jb) {
+                for (int jb = 0; jb < kQkJb; ++jb) {
                     kc[jb][0] = kn[jb][0];
                     kc[jb][1] = kn[jb][1];
                 }
@@ -1052,7 +1049,7 @@ hipError_t launch_qkt(const PlanView& p, int dtype, const void* q, int ldq, cons
     const int G = op_heads(p);
     const int grid = dtype == 1 ? op_grid(p, G) : persistent_grid(p.qkt_cap, 8);
     if (dtype == 1)
-        hipLaunchKernelGGL(k_qkt_bf16, dim3(grid), dim3(256), 0, s, pa, static_cast<const uint16_t*>(q), ldq,
+        hipLaunchKernelGGL(k_qkt_bf16, dim3(grid), dim3(kQkThreads), 0, s, pa, static_cast<const uint16_t*>(q), ldq,
                            static_cast<const uint16_t*>(k), ldk, scale, static_cast<uint16_t*>(scores), score_cap,
                            int(causal), G);
     else
