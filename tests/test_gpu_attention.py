@@ -84,6 +84,32 @@ def test_config2_bf16():
     _check_ops(wl.lengths, wl.cfg.heads, wl.tensors["q"], wl.tensors["k"], wl.tensors["v"], "bf16", 0.125)
 
 
+def test_unfused_operators_batch128_sampled_sequences():
+    # the batch-128, 16-head shape: the plan holds about 9.7k (sequence, 64-query,
+    # head) items, enough for the operators to group several heads per work item
+    # (and QK^T to prefetch the next head's Q block); every operator's output of
+    # a spread of whole sequences against the oracle run on that sequence alone
+    wl = make_workload(4, seed=0)
+    L, H = wl.lengths, wl.cfg.heads
+    d = H * 64
+    rng = np.random.default_rng(4)
+    T = wl.total_tokens
+    q, k, v = (random_storage(rng, (T, d), "bf16", 1.0) for _ in range(3))
+    print(f"unfused operators B={len(L)} T={T}", flush=True)
+    S, P, O = _run_unfused(L, H, q, k, v, "bf16", 0.125)
+    tok = np.concatenate([[0], np.cumsum(L)])
+    att = H * np.concatenate([[0], np.cumsum(L.astype(np.int64) ** 2)])
+    order = np.argsort(-L, kind="stable")
+    picks = sorted(set(np.linspace(0, len(L) - 1, 5).round().astype(int).tolist()) | {int(order[0]), int(order[-1])})
+    for b in picks:
+        Lb = L[b:b + 1]
+        qb, kb, vb = (a[tok[b]:tok[b + 1]] for a in (q, k, v))
+        Sb, Pb = S[att[b]:att[b + 1]], P[att[b]:att[b + 1]]
+        assert scores_close(Sb, oracle.qkt("bf16", Lb, H, 64, qb, d, kb, d, 0.125), Lb, H, "bf16"), ("QK^T", b)
+        assert scores_close(Pb, oracle.softmax("bf16", Lb, H, Sb), Lb, H, "bf16"), ("softmax", b)
+        assert close(O[tok[b]:tok[b + 1]], oracle.attn_v("bf16", Lb, H, 64, Pb, vb, d), "bf16", d), ("Attn.V", b)
+
+
 RAGGED = [
     [1, 15, 16, 17, 63, 64, 65, 127, 129, 200],
     [0, 7, 0, 300, 2],
