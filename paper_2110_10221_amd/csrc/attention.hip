@@ -159,7 +159,7 @@ __global__ __launch_bounds__(kQkThreads) void k_qkt_bf16(PlanArgs pa, const uint
     __shared__ __attribute__((aligned(16))) uint16_t qs[2][kTile * kHeadDim];  // a head's Q block, two buffers
     const int H = pa.heads;
     const int n_items = pa.status[2] / G, ng = H / G;
-    const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
+    const int wave = uni(threadIdx.x / kWave), lane = threadIdx.x % kWave;
     const int l16 = lane % 16, q4 = lane / 16;
     for (int base_it = 0; base_it < n_items; base_it += gridDim.x) {
         const int g = base_it + op_item(blockIdx.x, gridDim.x);
@@ -425,7 +425,9 @@ __global__ __launch_bounds__(256) void k_softmax(PlanArgs pa, const typename Ele
                                                   typename Elem<BF16>::T* P, int64_t score_cap, int T, int causal) {
     using E = Elem<BF16>;
     if (!plan_ok(pa, score_cap)) return;
-    const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
+    // wave-uniform by construction; made explicit so that the token's offsets and
+    // the score rows' buffer descriptor stay in scalar registers
+    const int wave = uni(threadIdx.x / kWave), lane = threadIdx.x % kWave;
     const int t = blockIdx.x * 4 + wave;
     if (t >= T) return;
     const int b = pa.tok_seq[t];
