@@ -486,6 +486,17 @@ __device__ __forceinline__ void gemm_tile_bf16(const uint16_t* __restrict__ x, i
         // LDS all at once (BM rows of 512 bytes, 16-byte chunk c of row r at
         // physical chunk c ^ (r & 31)), then whole rows stored
         uint32_t* eb = reinterpret_cast<uint32_t*>(smem);
+        // the wave's bias groups, all loaded before the first is used (one wait, not
+        // one per group); features past N read a group in range and count as zero
+        u32x2 braw[FN][4];
+        if constexpr (HAS_BIAS) {
+#pragma unroll
+            for (int i = 0; i < FN; ++i)
+#pragma unroll
+                for (int g = 0; g < 4; ++g)
+                    braw[i][g] = *reinterpret_cast<const u32x2*>(
+                        bias + min(n0 + wn * WN + i * 32 + 8 * g + 4 * h2, N - 4));
+        }
         barrier_lds();  // the K loop is done with LDS
 #pragma unroll
         for (int i = 0; i < FN; ++i)
@@ -494,13 +505,11 @@ __device__ __forceinline__ void gemm_tile_bf16(const uint16_t* __restrict__ x, i
                 const int f0 = wn * WN + i * 32 + 8 * g + 4 * h2;  // feature (in the tile) of acc[.][.][4g]
                 float bv[4] = {0.f, 0.f, 0.f, 0.f};
                 if constexpr (HAS_BIAS) {
-                    if (n0 + f0 < N) {
-                        const u32x2 bb = *reinterpret_cast<const u32x2*>(bias + n0 + f0);
-                        bv[0] = lo_bf16(bb[0]);
-                        bv[1] = hi_bf16(bb[0]);
-                        bv[2] = lo_bf16(bb[1]);
-                        bv[3] = hi_bf16(bb[1]);
-                    }
+                    const u32x2 bb = n0 + f0 < N ? braw[i][g] : u32x2{0u, 0u};
+                    bv[0] = lo_bf16(bb[0]);
+                    bv[1] = hi_bf16(bb[0]);
+                    bv[2] = lo_bf16(bb[1]);
+                    bv[3] = hi_bf16(bb[1]);
                 }
 #pragma unroll
                 for (int j = 0; j < FM; ++j) {
@@ -541,15 +550,19 @@ __device__ __forceinline__ void gemm_tile_bf16(const uint16_t* __restrict__ x, i
     const int ncol = n0 + 8 * cl;    // its eight output features
     float bv[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
     if constexpr (HAS_BIAS) {
-        if (ncol < N) {  // two 8-byte loads: the bias need only be 8-byte aligned
+        // two 8-byte loads (the bias need only be 8-byte aligned), unconditional so
+        // that they go out with the residual loads below rather than waited for alone;
+        // features past N read a group in range and count as zero
+        u32x2 bb[2];
 #pragma unroll
-            for (int hb = 0; hb < 2; ++hb) {
-                const u32x2 bb = *reinterpret_cast<const u32x2*>(bias + ncol + 4 * hb);
-                bv[4 * hb] = lo_bf16(bb[0]);
-                bv[4 * hb + 1] = hi_bf16(bb[0]);
-                bv[4 * hb + 2] = lo_bf16(bb[1]);
-                bv[4 * hb + 3] = hi_bf16(bb[1]);
-            }
+        for (int hb = 0; hb < 2; ++hb) bb[hb] = *reinterpret_cast<const u32x2*>(bias + min(ncol, N - 8) + 4 * hb);
+#pragma unroll
+        for (int hb = 0; hb < 2; ++hb) {
+            const u32x2 b2 = ncol < N ? bb[hb] : u32x2{0u, 0u};
+            bv[4 * hb] = lo_bf16(b2[0]);
+            bv[4 * hb + 1] = hi_bf16(b2[0]);
+            bv[4 * hb + 2] = lo_bf16(b2[1]);
+            bv[4 * hb + 3] = hi_bf16(b2[1]);
         }
     }
     constexpr int kRowsPerWave = kEpiRows / (C::kWaves * GROUPS);
