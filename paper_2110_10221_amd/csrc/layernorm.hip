@@ -53,13 +53,25 @@ __global__ __launch_bounds__(256) void k_layernorm(const void* x, int ldx, const
     const int row = blockIdx.x * 4 + wave;
     if (row >= T) return;
     const int nch = d / E;
-    float v[MAXC][E];
+    // Every load is issued before the first value is used (one wait for all of
+    // them): chunk indexes are clamped into the row and lanes past it ignore what
+    // they read.  gamma and beta join them while the registers allow.
+    constexpr bool kEarlyGB = MAXC <= 4;
+    constexpr int kGB = kEarlyGB ? MAXC : 1;
+    float v[MAXC][E], g[kGB][E], bt[kGB][E];
+#pragma unroll
+    for (int c = 0; c < MAXC; ++c) {
+        const int ch = min(lane + kWave * c, nch - 1);
+        IO::load(x, (int64_t)row * ldx + ch * E, v[c]);
+        if constexpr (kEarlyGB) {
+            IO::load(gamma, ch * E, g[c]);
+            IO::load(beta, ch * E, bt[c]);
+        }
+    }
     float s = 0.f;
 #pragma unroll
     for (int c = 0; c < MAXC; ++c) {
-        const int ch = lane + kWave * c;
-        if (ch < nch) {
-            IO::load(x, (int64_t)row * ldx + ch * E, v[c]);
+        if (lane + kWave * c < nch) {
 #pragma unroll
             for (int e = 0; e < E; ++e) s += v[c][e];
         }
@@ -82,11 +94,14 @@ __global__ __launch_bounds__(256) void k_layernorm(const void* x, int ldx, const
     for (int c = 0; c < MAXC; ++c) {
         const int ch = lane + kWave * c;
         if (ch < nch) {
-            float g[E], bt[E], o[E];
-            IO::load(gamma, ch * E, g);
-            IO::load(beta, ch * E, bt);
+            const int cg = kEarlyGB ? c : 0;
+            if constexpr (!kEarlyGB) {
+                IO::load(gamma, ch * E, g[0]);
+                IO::load(beta, ch * E, bt[0]);
+            }
+            float o[E];
 #pragma unroll
-            for (int e = 0; e < E; ++e) o[e] = g[e] * ((v[c][e] - mean) * inv) + bt[e];
+            for (int e = 0; e < E; ++e) o[e] = g[cg][e] * ((v[c][e] - mean) * inv) + bt[cg][e];
             IO::store(y, (int64_t)row * ldy + ch * E, o);
         }
     }
