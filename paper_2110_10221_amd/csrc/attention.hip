@@ -210,14 +210,15 @@ __global__ __launch_bounds__(kQkThreads) void k_qkt_bf16(PlanArgs pa, const uint
                 const int j = f / npc;
                 asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
                 __syncthreads();
-                if (j + 1 < G) copy_q(j + 1);  // qs[(j + 1) & 1] was last read by head j - 1
-                // its Q fragments, rows rg*16 + l16
+                // its Q fragments, rows rg*16 + l16, read before the next head's copy goes
+                // out (an LDS read after a pending LDS copy waits for the copy)
                 const uint16_t* qb = qs[j & 1];
 #pragma unroll
                 for (int rg = 0; rg < 4; ++rg) {
                     qf[rg][0] = as_bf16x8(*reinterpret_cast<const u32x4*>(qb + kv_off(rg * 16 + l16, 8 * q4)));
                     qf[rg][1] = as_bf16x8(*reinterpret_cast<const u32x4*>(qb + kv_off(rg * 16 + l16, 32 + 8 * q4)));
                 }
+                if (j + 1 < G) copy_q(j + 1);  // qs[(j + 1) & 1] was last read by head j - 1
             }
             if (f + 1 < F) load_k(f + 1, kn);
             const int pn = min(kPiece, kend - p0);
@@ -262,8 +263,19 @@ __global__ __launch_bounds__(kQkThreads) void k_qkt_bf16(PlanArgs pa, const uint
                     const uint32_t rb = (sh & 1) * 2;
                     uint16_t* const dst = S + 8 * fa;
                     for (int cc = sub; cc < nch; cc += 8) {
-                        const uint32_t* d = src + 4 * cc;
-                        const uint32_t d0 = d[0], d1 = d[1], d2 = d[2], d3 = d[3], d4 = d[4];
+                        // the five dwords by LDS reads the compiler does not see, so it adds
+                        // no wait for the Q copy that may be in flight (it cannot tell the
+                        // buffers apart)
+                        const uint32_t da = (uint32_t)(uintptr_t)(src + 4 * cc);
+                        u32x2 d01, d23;
+                        uint32_t d4;
+                        asm volatile(
+                            "ds_read2_b32 %0, %3 offset1:1\n\tds_read2_b32 %1, %3 offset0:2 offset1:3\n\t"
+                            "ds_read_b32 %2, %3 offset:16\n\ts_waitcnt lgkmcnt(0)"
+                            : "=&v"(d01), "=&v"(d23), "=&v"(d4)
+                            : "v"(da)
+                            : "memory");
+                        const uint32_t d0 = d01[0], d1 = d01[1], d2 = d23[0], d3 = d23[1];
                         *reinterpret_cast<u32x4*>(dst + 8 * cc) =
                             u32x4{__builtin_amdgcn_alignbyte(d1, d0, rb), __builtin_amdgcn_alignbyte(d2, d1, rb),
                                   __builtin_amdgcn_alignbyte(d3, d2, rb), __builtin_amdgcn_alignbyte(d4, d3, rb)};
@@ -621,14 +633,14 @@ __global__ __launch_bounds__(256) void k_attn_v_bf16(PlanArgs pa, const uint16_t
             // this wave's copies of tile f, then every wave's; buffers f + 1 were last read in step f - 1
             asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
             asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
-            if (f + 1 < F) {
-                copy_v(f + 1, std::integral_constant<int, 1 - BUF>{});
-                copy_p(f + 1, std::integral_constant<int, 1 - BUF>{});
-            }
+            // This tile's probability pieces are read before tile f + 1's copies go
+            // out: the compiler makes an LDS read wait for every LDS copy in flight,
+            // which would hold the tile for the next one's copies.
             const int sh = (int)((e_lo - e_al + row_e0 + (int64_t)h * L + j0) & 7);
             const uint32_t rb = (sh & 1) * 2;
             const uint32_t* const prow =
                 reinterpret_cast<const uint32_t*>(pb + BUF * kAvPBuf) + (wave * 16 + l16) * (kAvPRow * 4) + (sh >> 1);
+            bf16x8 pk[2];
 #pragma unroll
             for (int ks = 0; ks < 2; ++ks) {
                 const int jk = j0 + 32 * ks + 8 * q4;
@@ -644,7 +656,15 @@ __global__ __launch_bounds__(256) void k_attn_v_bf16(PlanArgs pa, const uint16_t
                                           (row_ok && j + 1 <= kmax ? 0xffff0000u : 0u);
                     pw[e] &= keep;
                 }
-                const bf16x8 pb = as_bf16x8(pw);
+                pk[ks] = as_bf16x8(pw);
+            }
+            if (f + 1 < F) {
+                copy_v(f + 1, std::integral_constant<int, 1 - BUF>{});
+                copy_p(f + 1, std::integral_constant<int, 1 - BUF>{});
+            }
+#pragma unroll
+            for (int ks = 0; ks < 2; ++ks) {
+                const bf16x8 pb = pk[ks];
                 u32x2 t[4][2];
                 asm volatile(
                     "ds_read_b64_tr_b16 %0, %8 offset:%16\n\t"
