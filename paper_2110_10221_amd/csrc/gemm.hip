@@ -549,21 +549,14 @@ __device__ __forceinline__ void gemm_tile_bf16(const uint16_t* __restrict__ x, i
     const int cl = lane % 32;        // this lane's 16-byte output chunk of a row in the row phase
     const int ncol = n0 + 8 * cl;    // its eight output features
     float bv[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+    // two 8-byte bias loads (the bias need only be 8-byte aligned), unconditional so
+    // that they go out with the residual loads below; features past N read a group in
+    // range and count as zero.  They are unpacked only after the first slice is
+    // staged, so that their wait (and the residual loads' behind them) falls there.
+    u32x2 bb[2] = {u32x2{0u, 0u}, u32x2{0u, 0u}};
     if constexpr (HAS_BIAS) {
-        // two 8-byte loads (the bias need only be 8-byte aligned), unconditional so
-        // that they go out with the residual loads below rather than waited for alone;
-        // features past N read a group in range and count as zero
-        u32x2 bb[2];
 #pragma unroll
         for (int hb = 0; hb < 2; ++hb) bb[hb] = *reinterpret_cast<const u32x2*>(bias + min(ncol, N - 8) + 4 * hb);
-#pragma unroll
-        for (int hb = 0; hb < 2; ++hb) {
-            const u32x2 b2 = ncol < N ? bb[hb] : u32x2{0u, 0u};
-            bv[4 * hb] = lo_bf16(b2[0]);
-            bv[4 * hb + 1] = hi_bf16(b2[0]);
-            bv[4 * hb + 2] = lo_bf16(b2[1]);
-            bv[4 * hb + 3] = hi_bf16(b2[1]);
-        }
     }
     constexpr int kRowsPerWave = kEpiRows / (C::kWaves * GROUPS);
     constexpr int kRowPairs = kRowsPerWave / 2;  // wave instructions per slice: rows 2 p + h2
@@ -593,6 +586,19 @@ __device__ __forceinline__ void gemm_tile_bf16(const uint16_t* __restrict__ x, i
                 *reinterpret_cast<floatx4*>(ep_mine + (l32 * 64 + (c ^ l32)) * 4) = o;
             }
         barrier_lds();
+        if constexpr (HAS_BIAS) {
+            if (slice == 0) {
+                asm volatile("" : "+v"(bb[0]), "+v"(bb[1]));  // not before this point
+#pragma unroll
+                for (int hb = 0; hb < 2; ++hb) {
+                    const u32x2 b2 = ncol < N ? bb[hb] : u32x2{0u, 0u};
+                    bv[4 * hb] = lo_bf16(b2[0]);
+                    bv[4 * hb + 1] = hi_bf16(b2[0]);
+                    bv[4 * hb + 2] = lo_bf16(b2[1]);
+                    bv[4 * hb + 3] = hi_bf16(b2[1]);
+                }
+            }
+        }
 #pragma unroll
         for (int rp = 0; rp < kRowPairs; ++rp) {
             const int r = wave_all * kRowsPerWave + 2 * rp + h2;
