@@ -832,26 +832,46 @@ void k_gemm_f32_mfma(const float* __restrict__ x, int ldx, const float* __restri
                         acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[i][st], bq[j][st], acc[i][j], 0, 0, 0);
         }
     }
-    // acc[i][j][4g + r]: token wm*64 + j*32 + l32, feature wn*64 + i*32 + 8g + 4 h2 + r
+    // acc[i][j][4g + r]: token wm*64 + j*32 + l32, feature wn*64 + i*32 + 8g + 4 h2 + r.
+    // The bias groups, and per 32-feature block the residual chunks, are loaded
+    // before their first use (indexes clamped into range; one wait for each batch):
+    // loaded under the range tests, each was waited for before the next was issued.
+    floatx4 bv[2][4];
 #pragma unroll
     for (int i = 0; i < 2; ++i)
 #pragma unroll
         for (int g = 0; g < 4; ++g) {
+            bv[i][g] = floatx4{0.f, 0.f, 0.f, 0.f};
+            if constexpr (HB) bv[i][g] = *reinterpret_cast<const floatx4*>(bias + min(n0 + wn * 64 + i * 32 + 8 * g + 4 * h2, N - 4));
+        }
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+        floatx4 rv[4][2];
+        if constexpr (HR) {
+#pragma unroll
+            for (int g = 0; g < 4; ++g)
+#pragma unroll
+                for (int j = 0; j < 2; ++j)
+                    rv[g][j] = *reinterpret_cast<const floatx4*>(
+                        residual + (int64_t)min(m0 + wm * 64 + j * 32 + l32, T - 1) * ldr +
+                        min(n0 + wn * 64 + i * 32 + 8 * g + 4 * h2, N - 4));
+        }
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
             const int n = n0 + wn * 64 + i * 32 + 8 * g + 4 * h2;
             if (n >= N) continue;
-            floatx4 bv = {0.f, 0.f, 0.f, 0.f};
-            if constexpr (HB) bv = *reinterpret_cast<const floatx4*>(bias + n);
 #pragma unroll
             for (int j = 0; j < 2; ++j) {
                 const int m = m0 + wm * 64 + j * 32 + l32;
                 if (m >= T) continue;
                 floatx4 o;
 #pragma unroll
-                for (int r = 0; r < 4; ++r) o[r] = activate<ACT>(acc[i][j][4 * g + r] + bv[r]);
-                if constexpr (HR) o += *reinterpret_cast<const floatx4*>(residual + (int64_t)m * ldr + n);
+                for (int r = 0; r < 4; ++r) o[r] = activate<ACT>(acc[i][j][4 * g + r] + bv[i][g][r]);
+                if constexpr (HR) o += rv[g][j];
                 *reinterpret_cast<floatx4*>(y + (int64_t)m * ldy + n) = o;
             }
         }
+    }
 }
 
 template <int ACT, bool HB, bool HR>
