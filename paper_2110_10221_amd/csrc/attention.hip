@@ -115,29 +115,6 @@ __device__ __forceinline__ int op_item(int bid, int grid) {  // grid: a multiple
     return ((j / kOpRun) * 8 + xcd) * kOpRun + j % kOpRun;
 }
 
-// Elements s .. s + 7 of the 16 elements a:b (s in [0, 8)), i.e. bytes [2s, 2s + 16).
-__device__ __forceinline__ u32x4 window16(const u32x4& a, const u32x4& b, int s) {
-    const int q = s >> 1;
-    uint32_t d[5];
-#pragma unroll
-    for (int k = 0; k < 5; ++k) {
-        const uint32_t w0 = k < 4 ? a[k] : b[k - 4];
-        const uint32_t w1 = k + 1 < 4 ? a[k + 1] : b[k - 3];
-        const uint32_t w2 = k + 2 < 4 ? a[k + 2] : b[k - 2];
-        const uint32_t w3 = k + 3 < 4 ? a[k + 3] : b[k - 1];
-        d[k] = q == 0 ? w0 : q == 1 ? w1 : q == 2 ? w2 : w3;
-    }
-    u32x4 o;
-    if (s & 1) {
-#pragma unroll
-        for (int k = 0; k < 4; ++k) o[k] = __builtin_amdgcn_alignbyte(d[k + 1], d[k], 2);
-    } else {
-#pragma unroll
-        for (int k = 0; k < 4; ++k) o[k] = d[k];
-    }
-    return o;
-}
-
 // bf16 QK^T.  Per head of the item and piece of kPiece keys, wave w computes the
 // piece's key tile w for all 64 query rows of the block (v_mfma_f32_16x16x32_bf16,
 // K fragments straight from memory, the next piece's tile loaded while this one
@@ -158,7 +135,7 @@ __global__ __launch_bounds__(kQkThreads) void k_qkt_bf16(PlanArgs pa, const uint
     __shared__ __attribute__((aligned(16))) uint16_t st[kTile][kPieceRow];
     __shared__ __attribute__((aligned(16))) uint16_t qs[2][kTile * kHeadDim];  // a head's Q block, two buffers
     const int H = pa.heads;
-    const int n_items = pa.status[2] / G, ng = H / G;
+    const int n_items = pa.status[2] / G;
     const int wave = uni(threadIdx.x / kWave), lane = threadIdx.x % kWave;
     const int l16 = lane % 16, q4 = lane / 16;
     for (int base_it = 0; base_it < n_items; base_it += gridDim.x) {
