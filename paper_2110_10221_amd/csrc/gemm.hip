@@ -759,47 +759,54 @@ __global__ __launch_bounds__(256) void k_gemm_f32(const float* __restrict__ x, i
 // both operands), so one 16-byte LDS read feeds four MFMAs.  The MFMA computes
 // C^T = W X^T: a lane holds four consecutive output features of one token,
 // stored as one 16-byte vector.
-constexpr int kF32M = 128, kF32N = 128, kF32K = 32;
-constexpr int kF32StageFloats = (kF32M + kF32N) * kF32K;
-constexpr int kF32Lds = 2 * kF32StageFloats * 4;
+constexpr int kF32K = 32;
+template <int TS>
+constexpr int f32_stage_floats() { return 2 * TS * kF32K; }  // TS x rows, then TS w rows
 
-template <int ACT, bool HB, bool HR>
+// TS = 128 (four waves of 64 x 64) or, for launches that would leave most CUs
+// idle, TS = 64 (four waves of 32 x 32: four times the tiles; a wave's single
+// accumulator chain still issues an fp32 MFMA every cycle the pipe allows).
+template <int ACT, bool HB, bool HR, int TS>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void k_gemm_f32_mfma(const float* __restrict__ x, int ldx, const float* __restrict__ w,
                      const float* __restrict__ bias, const float* residual, int ldr, float* y, int ldy, int T,
                      int K, int N, int tiles_m, int tiles_n) {
+    static_assert(TS == 128 || TS == 64, "tile side");
+    constexpr int WS = TS / 2, F = WS / 32;          // the wave's sub-tile side and 32-wide blocks
+    constexpr int kStage = f32_stage_floats<TS>();
+    constexpr int kBx = TS / 8, kPerWave = 2 * kBx / 4;  // 1 KB x blocks; copies per wave and step
     extern __shared__ __attribute__((aligned(16))) float fsm[];
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave), lane = threadIdx.x % kWave;
     const int l32 = lane % 32, h2 = lane / 32;
-    const int wm = wave >> 1, wn = wave & 1;  // the wave's 64 tokens and 64 features
+    const int wm = wave >> 1, wn = wave & 1;  // the wave's WS tokens and WS features
     int tm, tn;
     tile_coords(blockIdx.x, gridDim.x, tiles_m, tiles_n, tm, tn);
-    const int m0 = tm * kF32M, n0 = tn * kF32N;
-    const __amdgpu_buffer_rsrc_t rx = make_rsrc(x + (int64_t)m0 * ldx, (uint32_t)min(T - m0, kF32M) * ldx * 4u);
-    const __amdgpu_buffer_rsrc_t rw = make_rsrc(w + (int64_t)n0 * K, (uint32_t)min(N - n0, kF32N) * K * 4u);
-    // copy block b (1 KB: 8 rows of 128 bytes; blocks 0-15 x rows, 16-31 w rows):
-    // this wave fills blocks 8 wave .. 8 wave + 7, lane l slot l (row 8 b' + l / 8,
+    const int m0 = tm * TS, n0 = tn * TS;
+    const __amdgpu_buffer_rsrc_t rx = make_rsrc(x + (int64_t)m0 * ldx, (uint32_t)min(T - m0, TS) * ldx * 4u);
+    const __amdgpu_buffer_rsrc_t rw = make_rsrc(w + (int64_t)n0 * K, (uint32_t)min(N - n0, TS) * K * 4u);
+    // copy block b (1 KB: 8 rows of 128 bytes; blocks 0 .. kBx - 1 x rows, then w rows):
+    // this wave fills blocks kPerWave wave .. + kPerWave - 1, lane l slot l (row 8 b' + l / 8,
     // physical chunk l % 8, which holds logical chunk (l % 8) ^ swz2(row))
-    int voff[8];
+    int voff[8];  // first kPerWave used (a size that depends on TS made hipcc drop the host stub)
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
-        const int blk = wave * 8 + i, bl = blk & 15, row = bl * 8 + lane / 8;
-        voff[i] = row * (blk < 16 ? ldx : K) * 4 + ((lane % 8) ^ swz2(row)) * 16;
+    for (int i = 0; i < kPerWave; ++i) {
+        const int blk = wave * kPerWave + i, bl = blk % kBx, row = bl * 8 + lane / 8;
+        voff[i] = row * (blk < kBx ? ldx : K) * 4 + ((lane % 8) ^ swz2(row)) * 16;
     }
     auto issue = [&](int step) {
-        float* st = fsm + (step & 1) * kF32StageFloats;
+        float* st = fsm + (step & 1) * kStage;
 #pragma unroll
-        for (int i = 0; i < 8; ++i) {
-            const int blk = wave * 8 + i;
-            __builtin_amdgcn_raw_ptr_buffer_load_lds(blk < 16 ? rx : rw, (lds_void_t*)(st + blk * 256), 16, voff[i],
+        for (int i = 0; i < kPerWave; ++i) {
+            const int blk = wave * kPerWave + i;
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(blk < kBx ? rx : rw, (lds_void_t*)(st + blk * 256), 16, voff[i],
                                                      step * kF32K * 4, 0, 0);
         }
     };
-    floatx16 acc[2][2];
+    floatx16 acc[F][F];
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
+    for (int i = 0; i < F; ++i)
 #pragma unroll
-        for (int j = 0; j < 2; ++j)
+        for (int j = 0; j < F; ++j)
 #pragma unroll
             for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
     const int nk = K / kF32K;
@@ -808,61 +815,61 @@ void k_gemm_f32_mfma(const float* __restrict__ x, int ldx, const float* __restri
         wait_vm<0>();
         barrier_lds();  // step k's stage is visible; the other stage is no longer read
         if (k + 1 < nk) issue(k + 1);
-        const float* xs = fsm + (k & 1) * kF32StageFloats;
-        const float* ws = xs + kF32M * kF32K;
+        const float* xs = fsm + (k & 1) * kStage;
+        const float* ws = xs + TS * kF32K;
 #pragma unroll
         for (int gq = 0; gq < 4; ++gq) {
-            floatx4 a[2], bq[2];
+            floatx4 a[F], bq[F];
 #pragma unroll
-            for (int i = 0; i < 2; ++i) {
-                const int r = wn * 64 + i * 32 + l32;
+            for (int i = 0; i < F; ++i) {
+                const int r = wn * WS + i * 32 + l32;
                 a[i] = *reinterpret_cast<const floatx4*>(ws + r * kF32K + (((gq * 2 + h2) ^ swz2(r)) * 4));
             }
 #pragma unroll
-            for (int j = 0; j < 2; ++j) {
-                const int r = wm * 64 + j * 32 + l32;
+            for (int j = 0; j < F; ++j) {
+                const int r = wm * WS + j * 32 + l32;
                 bq[j] = *reinterpret_cast<const floatx4*>(xs + r * kF32K + (((gq * 2 + h2) ^ swz2(r)) * 4));
             }
 #pragma unroll
             for (int st = 0; st < 4; ++st)
 #pragma unroll
-                for (int i = 0; i < 2; ++i)
+                for (int i = 0; i < F; ++i)
 #pragma unroll
-                    for (int j = 0; j < 2; ++j)
+                    for (int j = 0; j < F; ++j)
                         acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[i][st], bq[j][st], acc[i][j], 0, 0, 0);
         }
     }
-    // acc[i][j][4g + r]: token wm*64 + j*32 + l32, feature wn*64 + i*32 + 8g + 4 h2 + r.
+    // acc[i][j][4g + r]: token wm*WS + j*32 + l32, feature wn*WS + i*32 + 8g + 4 h2 + r.
     // The bias groups, and per 32-feature block the residual chunks, are loaded
     // before their first use (indexes clamped into range; one wait for each batch):
     // loaded under the range tests, each was waited for before the next was issued.
-    floatx4 bv[2][4];
+    floatx4 bv[F][4];
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
+    for (int i = 0; i < F; ++i)
 #pragma unroll
         for (int g = 0; g < 4; ++g) {
             bv[i][g] = floatx4{0.f, 0.f, 0.f, 0.f};
-            if constexpr (HB) bv[i][g] = *reinterpret_cast<const floatx4*>(bias + min(n0 + wn * 64 + i * 32 + 8 * g + 4 * h2, N - 4));
+            if constexpr (HB) bv[i][g] = *reinterpret_cast<const floatx4*>(bias + min(n0 + wn * WS + i * 32 + 8 * g + 4 * h2, N - 4));
         }
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
-        floatx4 rv[4][2];
+    for (int i = 0; i < F; ++i) {
+        floatx4 rv[4][F];
         if constexpr (HR) {
 #pragma unroll
             for (int g = 0; g < 4; ++g)
 #pragma unroll
-                for (int j = 0; j < 2; ++j)
+                for (int j = 0; j < F; ++j)
                     rv[g][j] = *reinterpret_cast<const floatx4*>(
-                        residual + (int64_t)min(m0 + wm * 64 + j * 32 + l32, T - 1) * ldr +
-                        min(n0 + wn * 64 + i * 32 + 8 * g + 4 * h2, N - 4));
+                        residual + (int64_t)min(m0 + wm * WS + j * 32 + l32, T - 1) * ldr +
+                        min(n0 + wn * WS + i * 32 + 8 * g + 4 * h2, N - 4));
         }
 #pragma unroll
         for (int g = 0; g < 4; ++g) {
-            const int n = n0 + wn * 64 + i * 32 + 8 * g + 4 * h2;
+            const int n = n0 + wn * WS + i * 32 + 8 * g + 4 * h2;
             if (n >= N) continue;
 #pragma unroll
-            for (int j = 0; j < 2; ++j) {
-                const int m = m0 + wm * 64 + j * 32 + l32;
+            for (int j = 0; j < F; ++j) {
+                const int m = m0 + wm * WS + j * 32 + l32;
                 if (m >= T) continue;
                 floatx4 o;
 #pragma unroll
@@ -874,20 +881,31 @@ void k_gemm_f32_mfma(const float* __restrict__ x, int ldx, const float* __restri
     }
 }
 
-template <int ACT, bool HB, bool HR>
-hipError_t launch_f32_mfma(const float* x, int ldx, const float* w, const float* bias, const float* residual, int ldr,
-                           float* y, int ldy, int T, int K, int N, hipStream_t s) {
+template <int ACT, bool HB, bool HR, int TS>
+hipError_t launch_f32_mfma_ts(const float* x, int ldx, const float* w, const float* bias, const float* residual,
+                              int ldr, float* y, int ldy, int T, int K, int N, hipStream_t s) {
+    constexpr int kLds = 2 * f32_stage_floats<TS>() * 4;
     static bool attr_set = false;  // benign race: every thread sets the same value
     if (!attr_set) {
-        hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_gemm_f32_mfma<ACT, HB, HR>),
-                                           hipFuncAttributeMaxDynamicSharedMemorySize, kF32Lds);
+        hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_gemm_f32_mfma<ACT, HB, HR, TS>),
+                                           hipFuncAttributeMaxDynamicSharedMemorySize, kLds);
         if (e != hipSuccess) return e;
         attr_set = true;
     }
-    const int tiles_m = (T + kF32M - 1) / kF32M, tiles_n = (N + kF32N - 1) / kF32N;
-    hipLaunchKernelGGL((k_gemm_f32_mfma<ACT, HB, HR>), dim3(tiles_m * tiles_n), dim3(256), kF32Lds, s, x, ldx, w, bias,
-                       residual, ldr, y, ldy, T, K, N, tiles_m, tiles_n);
+    const int tiles_m = (T + TS - 1) / TS, tiles_n = (N + TS - 1) / TS;
+    hipLaunchKernelGGL((k_gemm_f32_mfma<ACT, HB, HR, TS>), dim3(tiles_m * tiles_n), dim3(256), kLds, s, x, ldx, w,
+                       bias, residual, ldr, y, ldy, T, K, N, tiles_m, tiles_n);
     return hipGetLastError();
+}
+
+// 128 x 128 tiles unless they would occupy at most half the CUs
+template <int ACT, bool HB, bool HR>
+hipError_t launch_f32_mfma(const float* x, int ldx, const float* w, const float* bias, const float* residual, int ldr,
+                           float* y, int ldy, int T, int K, int N, hipStream_t s) {
+    const int64_t tiles128 = (int64_t)((T + 127) / 128) * ((N + 127) / 128);
+    if (2 * tiles128 <= device_cu_count())
+        return launch_f32_mfma_ts<ACT, HB, HR, 64>(x, ldx, w, bias, residual, ldr, y, ldy, T, K, N, s);
+    return launch_f32_mfma_ts<ACT, HB, HR, 128>(x, ldx, w, bias, residual, ldr, y, ldy, T, K, N, s);
 }
 
 template <int ACT>
