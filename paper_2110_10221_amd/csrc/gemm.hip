@@ -898,12 +898,17 @@ hipError_t launch_f32_mfma_ts(const float* x, int ldx, const float* w, const flo
     return hipGetLastError();
 }
 
-// 128 x 128 tiles unless they would occupy at most half the CUs
+// 64 x 64 tiles when they cut the busiest CU's share of work, counted in rounds of
+// one tile per CU (a 128 x 128 tile being four 64 x 64 ones), by a fifth or more:
+// they re-read each operand twice as often, which large launches notice (35475 x
+// 1024 x 4096: 139 rounds of 64 x 64 against 35 of 128 x 128 ran 7% slower)
 template <int ACT, bool HB, bool HR>
 hipError_t launch_f32_mfma(const float* x, int ldx, const float* w, const float* bias, const float* residual, int ldr,
                            float* y, int ldy, int T, int K, int N, hipStream_t s) {
+    const int64_t cus = device_cu_count();
     const int64_t tiles128 = (int64_t)((T + 127) / 128) * ((N + 127) / 128);
-    if (2 * tiles128 <= device_cu_count())
+    const int64_t tiles64 = (int64_t)((T + 63) / 64) * ((N + 63) / 64);
+    if (5 * ((tiles64 + cus - 1) / cus) <= 16 * ((tiles128 + cus - 1) / cus))
         return launch_f32_mfma_ts<ACT, HB, HR, 64>(x, ldx, w, bias, residual, ldr, y, ldy, T, K, N, s);
     return launch_f32_mfma_ts<ACT, HB, HR, 128>(x, ldx, w, bias, residual, ldr, y, ldy, T, K, N, s);
 }

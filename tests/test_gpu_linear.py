@@ -56,12 +56,13 @@ def test_ragged_token_counts(T, K, N):
 @pytest.mark.parametrize("T,K,N,act,res", [(2236, 2048, 512, oracle.ACT_NONE, True),
                                            (2236, 512, 2048, oracle.ACT_GELU_ERF, False),
                                            (1001, 1024, 320, oracle.ACT_NONE, True),
-                                           (5000, 256, 1024, oracle.ACT_NONE, True)])
+                                           (5000, 256, 1024, oracle.ACT_NONE, True),
+                                           (4096, 256, 2048, oracle.ACT_GELU_TANH, True)])
 def test_f32_small_and_large_launches(T, K, N, act, res):
-    # fp32 on the matrix cores: launches whose 128 x 128 tiles would fill at most half
-    # the CUs run 64 x 64 tiles (the batch-32 lognormal FF2 shape, 1001 x 320 with a
-    # ragged tail of tokens and features), larger ones keep 128 x 128 (the FF1 shape,
-    # 5000 tokens: 320 tiles); sampled rows
+    # fp32 on the matrix cores, 64 x 64 tiles where they leave the busiest CU less
+    # work (the batch-32 lognormal FF2 and FF1 shapes, 1001 x 320 with a ragged tail of
+    # tokens and features, 5000 tokens: 320 tiles of 128 x 128 on 256 CUs), 128 x 128
+    # tiles otherwise (4096 x 2048: 512 tiles, two full rounds); sampled rows
     rows = np.r_[0:16, T // 2:T // 2 + 16, T - 16:T]
     got, ref = _linear("f32", T, K, N, act, True, res, seed=T + K, rows=rows)
     assert close(got, ref, "f32", N)
