@@ -712,13 +712,22 @@ __global__ __launch_bounds__(256) void k_attn_v_f32(PlanArgs pa, const float* __
         const int jend = causal ? min(L, (ti + 1) * kTile) : L;
         for (int j0 = 0; j0 < jend; j0 += kTile) {
             const int cols = min(kTile, L - j0);
-            __syncthreads();
-            for (int e = threadIdx.x; e < kTile * kTile; e += 256) {
-                const int r = e / kTile, c = e % kTile;
-                Ps[r][c] = (r < rows && c < cols && (!causal || j0 + c <= ti * kTile + r))
-                               ? P[base + ((int64_t)(ti * kTile + r) * H + h) * L + j0 + c]
-                               : 0.f;
-                Vs[r][c] = r < cols ? v[(int64_t)(t0 + j0 + r) * ldv + h * kHeadDim + c] : 0.f;
+            // every load unconditional at an index clamped into the block, the masked
+            // elements zeroed afterwards: loads under the range tests were each waited
+            // for before the next was issued
+            float pv[kTile * kTile / 256], vv[kTile * kTile / 256];
+#pragma unroll
+            for (int u = 0; u < kTile * kTile / 256; ++u) {
+                const int e = threadIdx.x + 256 * u, r = e / kTile, c = e % kTile;
+                pv[u] = P[base + ((int64_t)(ti * kTile + min(r, rows - 1)) * H + h) * L + j0 + min(c, cols - 1)];
+                vv[u] = v[(int64_t)(t0 + j0 + min(r, cols - 1)) * ldv + h * kHeadDim + c];
+            }
+            __syncthreads();  // the previous block's operand reads are done
+#pragma unroll
+            for (int u = 0; u < kTile * kTile / 256; ++u) {
+                const int e = threadIdx.x + 256 * u, r = e / kTile, c = e % kTile;
+                Ps[r][c] = (r < rows && c < cols && (!causal || j0 + c <= ti * kTile + r)) ? pv[u] : 0.f;
+                Vs[r][c] = r < cols ? vv[u] : 0.f;
             }
             __syncthreads();
 #pragma unroll 8
