@@ -365,6 +365,43 @@ def sdpa_measurement(rag, cid, seed=0, iters=30):
                         "qkt": "k_qkt_bf16", "softmax": "k_softmax<true>", "attn_v": "k_attn_v_bf16"}}
 
 
+def uniform_control_measurement(rag, iters=30):
+    """A control for the cost of raggedness (the overhead study of Section 7.4 and
+    Appendix D runs a batch of 64 sequences all of length 512): the batch-128 layer
+    shape (d_model 1024, 16 heads x 64, FFN 4096, bf16) on 64 sequences of exactly
+    512 tokens, so nothing is padded and every tile is full.  The layer runs with
+    its plan built inside the QKV projection's launch (as the bench line does) and
+    with the plan built once and reused; their difference is what the ragged
+    machinery costs per layer, and the useful rate beside the ragged batch-128 one
+    shows what the lengths' spread costs the kernels."""
+    import torch
+
+    from tests.helpers import dev
+    from workloads import BIAS_NAMES, CONFIGS, LN_NAMES, WEIGHT_NAMES, make_workload
+
+    wl = make_workload(4, seed=0)  # its weights; x is its first 32768 token rows
+    cfg = wl.cfg
+    d, H, dff = cfg.d_model, cfg.heads, cfg.d_ff
+    L = np.full(64, 512, dtype=np.int32)
+    T = int(L.sum())
+    plan = rag.Plan(torch.from_numpy(L).cuda(), T, 512, H)
+    x = dev(wl.tensors["x"], "bf16")[:T].contiguous()
+    wd = {n: dev(wl.tensors[n], "bf16") for n in WEIGHT_NAMES + BIAS_NAMES + LN_NAMES}
+    wstruct = rag.layer_weights(wd)
+    ws = torch.empty(rag.encoder_layer_workspace(T, 512, d, H, dff, rag.RAG_BF16, 0), dtype=torch.uint8,
+                     device="cuda")
+    y = torch.empty(T, d, dtype=torch.bfloat16, device="cuda")
+    ms = _timed(lambda: rag.encoder_layer(plan, x, y, wstruct, dff, ws, flags=rag.RAG_LAYER_BUILD_PLAN), iters)
+    ms_reused = _timed(lambda: rag.encoder_layer(plan, x, y, wstruct, dff, ws), iters)
+    assert not plan.data_errors(), plan.data_errors()
+    uf = useful_flops(L, d, dff)
+    return {"workload": f"batch 64, lengths fixed 512, {H} heads x 64, FFN {dff}, bf16, T = {T}",
+            "ms_per_layer": round(ms, 4), "ms_per_layer_plan_reused": round(ms_reused, 4),
+            "plan_share": round((ms - ms_reused) / ms, 4),
+            "useful_tflops": round(uf / (ms * 1e-3) / 1e12, 1),
+            "frac_of_bf16_peak": round(uf / (ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4)}
+
+
 def other_configs_measurement(rag, iters=30):
     """The other four configurations of the workload table, each on its own path:
     1 (fp32, operator-level SDPA: prelude + ragged_qkt + ragged_softmax +
@@ -762,6 +799,7 @@ def main():
         out["trmm"] = trmm_measurement(rag)
     if not args.no_configs:
         out["other_configs"] = other_configs_measurement(rag)
+        out["uniform_control"] = uniform_control_measurement(rag)
     if not args.no_peaks:
         out["measured_peaks"] = measured_peaks(rag)
     if not args.no_cpu_baseline:
